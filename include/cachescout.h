@@ -1,0 +1,167 @@
+/*
+ * cachescout.h - C ABI of libcachescout.so: paged prefix-reuse prefill
+ * attention and KV prefetch for AMD Instinct MI355X (gfx950).
+ *
+ * The two calls are the GPU work behind agent-aware KV-cache reuse
+ * (arXiv 2608.14624, "Learning Agent Execution for KV-Cache Management in
+ * Agentic Serving"):
+ *
+ *   cs_prefill_paged_attn  - an agent invocation that hits its cached prompt
+ *                            prefix (the "agent anchor", Sec. 2.1) runs
+ *                            attention for its new suffix tokens over the
+ *                            anchor's KV, which sits in 16-token blocks of a
+ *                            paged GPU pool (Sec. 2.1 "Prefix caching"), plus
+ *                            the suffix's own causal KV.  A miss is the same
+ *                            call with prefix length 0.
+ *   cs_kv_prefetch         - the predicted next agent's anchor blocks
+ *                            (Sec. 3.4, Eq. (10) picks that agent) are
+ *                            reloaded from the CPU tier into free pool slots
+ *                            (architecture figure of Sec. 3; Sec. 4), as a
+ *                            bit-exact block copy.
+ *
+ * Conventions shared by both calls
+ *   - Every pointer is caller-owned.  The library allocates no device or host
+ *     memory and keeps no state beyond a per-process cache of device
+ *     properties; calls are reentrant and may run concurrently on different
+ *     streams.
+ *   - Both calls enqueue their kernel on `stream` (NULL = the legacy default
+ *     stream of the current device) and return without synchronizing.  Device
+ *     metadata is read by the kernels, never by the host, so the calls can be
+ *     captured in a HIP graph (unless CS_DEBUG_CHECK=1, see below).
+ *   - The device is the caller's current HIP device; every device pointer
+ *     must belong to it.
+ *   - bf16 means IEEE-754 binary32 truncated to its upper 16 bits (bfloat16),
+ *     stored little-endian as 2 bytes.
+ *   - Return value: CS_OK, or one of the error codes below.  Arguments are
+ *     validated synchronously before anything is enqueued; on an error
+ *     nothing is launched.  cs_last_error() gives a message for the calling
+ *     thread's last failure.
+ *   - Values that live in device memory (block ids, lengths) are NOT checked
+ *     in normal operation; out-of-range or inconsistent values are undefined
+ *     behaviour.  With the environment variable CS_DEBUG_CHECK=1 the library
+ *     copies that metadata to the host, synchronizing the stream, and
+ *     validates it first (CS_ERR_INVALID_ARG on a violation).
+ */
+#ifndef CACHESCOUT_H
+#define CACHESCOUT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A HIP stream handle (hipStream_t) passed through as an opaque pointer. */
+typedef struct ihipStream_t *cs_stream_t;
+
+enum cs_status {
+    CS_OK = 0,
+    CS_ERR_INVALID_ARG = 1,  /* a null pointer, negative size, inconsistent
+                                sizes, misaligned buffer, non-pinned host
+                                buffer, or (debug mode) bad device metadata */
+    CS_ERR_UNSUPPORTED = 2,  /* valid but not implemented: head_dim other
+                                than 64 or 128, block_size other than 16 */
+    CS_ERR_HIP = 3           /* the HIP runtime reported an error */
+};
+
+/*
+ * Paged prefill attention with a reused prefix (GQA, variable length).
+ *
+ * Operation (Sec. 2.1 "Prefix caching": a hit reuses the prefix KV instead
+ * of recomputing it, so the result equals a full recompute): for every
+ * invocation r < batch, query head h < num_q_heads, suffix row
+ * i < S_r = cu_q_lens[r+1] - cu_q_lens[r] and feature d < head_dim,
+ *
+ *   P = prefix_lens[r],  g = h / (num_q_heads / num_kv_heads)
+ *   K_r[j] = k_pool[block_tables[r][j / 16]][g][j % 16][:]   (V_r likewise)
+ *   s_j    = scale * dot(q[cu_q_lens[r] + i][h][:], K_r[j])   for j <= P + i
+ *   out[cu_q_lens[r] + i][h][d] = sum_j softmax(s)_j * V_r[j][d]
+ *
+ * i.e. suffix row i is prompt position P + i and sees keys 0 .. P + i (the
+ * causal mask is aligned to the end of the prompt).  Every key, prefix or
+ * suffix, is read through the block table: the suffix's own K/V must already
+ * be in the pool.  Arithmetic: bf16 products with float32 accumulation,
+ * float32 softmax; the probabilities are rounded to bf16 before the product
+ * with V; the output is rounded to nearest-even bf16.
+ *
+ * Arguments
+ *   q             device, bf16 [total_q][num_q_heads][head_dim], the suffix
+ *                 tokens of all invocations packed in invocation order;
+ *                 16-byte aligned.
+ *   k_pool,
+ *   v_pool        device, bf16 [num_blocks][num_kv_heads][block_size][head_dim]
+ *                 (one (block, head) tile is contiguous); 16-byte aligned.
+ *   block_tables  device, int32 [batch][max_blocks_per_seq]; row r maps logical
+ *                 block b to a pool slot in [0, num_blocks) for
+ *                 b < ceil((P_r + S_r) / block_size); later entries are not read.
+ *                 Rows may share slots (a shared anchor).
+ *   prefix_lens   device, int32 [batch], P_r >= 0 (0 = a miss).
+ *   cu_q_lens     device, int32 [batch + 1], cu_q_lens[0] = 0, non-decreasing,
+ *                 cu_q_lens[batch] = total_q.  S_r = 0 is allowed.
+ *   batch, total_q          as above.
+ *   max_q_len     >= every S_r (host value; sizes the launch).
+ *   max_kv_len    >= every P_r + S_r; max_blocks_per_seq * block_size must be
+ *                 >= max_kv_len.
+ *   num_blocks    pool slots.
+ *   num_q_heads, num_kv_heads  num_q_heads % num_kv_heads == 0.
+ *   head_dim      64 or 128.   block_size  16.
+ *   scale         logit scale, finite (typically 1/sqrt(head_dim)).
+ *   out           device, bf16 [total_q][num_q_heads][head_dim], 16-byte
+ *                 aligned, must not overlap the inputs.
+ *   stream        HIP stream.
+ *
+ * batch == 0, total_q == 0 or max_q_len == 0 is a no-op returning CS_OK.
+ */
+int cs_prefill_paged_attn(const void *q, const void *k_pool, const void *v_pool,
+                          const int32_t *block_tables, const int32_t *prefix_lens,
+                          const int32_t *cu_q_lens, int32_t batch, int32_t total_q,
+                          int32_t max_q_len, int32_t max_kv_len,
+                          int32_t max_blocks_per_seq, int32_t num_blocks,
+                          int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                          int32_t block_size, float scale, void *out,
+                          cs_stream_t stream);
+
+/*
+ * KV prefetch: copy whole blocks from pinned host memory into pool slots.
+ *
+ * Operation (reload of an anchor from the CPU tier, Sec. 3 architecture
+ * figure and Sec. 4; the reloaded blocks are the ones a normal invocation
+ * produces, so the copy is bit-exact): for every i < n,
+ *   k_pool[dst_block_ids[i]] = host_k_blocks[i]
+ *   v_pool[dst_block_ids[i]] = host_v_blocks[i]
+ * byte for byte; no other slot is written.  The kernel reads the host
+ * buffers directly over the host link.
+ *
+ * Arguments
+ *   host_k_blocks,
+ *   host_v_blocks  pinned, device-mapped host memory (hipHostMalloc, or a
+ *                  PyTorch pin_memory tensor), bf16
+ *                  [n][num_kv_heads][block_size][head_dim], 16-byte aligned.
+ *                  Anything else -> CS_ERR_INVALID_ARG.
+ *   dst_block_ids  device, int32 [n]; unique, each in [0, num_blocks).
+ *   n              number of blocks; 0 is a no-op returning CS_OK.
+ *   k_pool, v_pool device, as in cs_prefill_paged_attn, 16-byte aligned.
+ *   num_blocks, num_kv_heads, head_dim (64 or 128), block_size (16).
+ *   stream         HIP stream, typically a side stream.  The destination
+ *                  slots must not be read or written by any kernel still in
+ *                  flight; order the consumer with an event recorded after
+ *                  this call.  The host buffers must stay alive and unchanged
+ *                  until the copy has completed.
+ */
+int cs_kv_prefetch(const void *host_k_blocks, const void *host_v_blocks,
+                   const int32_t *dst_block_ids, int32_t n, void *k_pool, void *v_pool,
+                   int32_t num_blocks, int32_t num_kv_heads, int32_t head_dim,
+                   int32_t block_size, cs_stream_t stream);
+
+/* Static, NUL-terminated name of a status code ("CS_OK", ...). */
+const char *cs_status_string(int status);
+
+/* Message describing the calling thread's most recent failed call; "" if none.
+ * The pointer stays valid until the thread's next call into the library. */
+const char *cs_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CACHESCOUT_H */

@@ -1,0 +1,230 @@
+// C ABI of libcachescout.so: argument validation, pinned-pointer resolution,
+// optional metadata checks (CS_DEBUG_CHECK=1) and kernel launches.  The
+// operations themselves are described in include/cachescout.h.
+#include "cachescout.h"
+#include "internal.h"
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+namespace {
+
+thread_local char g_last_error[512];
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int ok() {
+  g_last_error[0] = '\0';
+  return CS_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(CS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool debug_checks_enabled() {
+  const char* v = getenv("CS_DEBUG_CHECK");
+  return v != nullptr && v[0] == '1';
+}
+
+template <typename T>
+hipError_t copy_to_host(std::vector<T>& dst, const T* src, size_t count, hipStream_t stream) {
+  dst.resize(count);
+  if (count == 0) return hipSuccess;
+  hipError_t e = hipMemcpyAsync(dst.data(), src, count * sizeof(T), hipMemcpyDeviceToHost, stream);
+  if (e != hipSuccess) return e;
+  return hipStreamSynchronize(stream);
+}
+
+int debug_check_attn(const int32_t* block_tables, const int32_t* prefix_lens,
+                     const int32_t* cu_q_lens, int batch, int total_q, int max_q_len,
+                     int max_kv_len, int max_blocks_per_seq, int num_blocks,
+                     hipStream_t stream) {
+  std::vector<int32_t> cu, pl, bt;
+  hipError_t e = copy_to_host(cu, cu_q_lens, (size_t)batch + 1, stream);
+  if (e == hipSuccess) e = copy_to_host(pl, prefix_lens, (size_t)batch, stream);
+  if (e == hipSuccess) e = copy_to_host(bt, block_tables, (size_t)batch * max_blocks_per_seq, stream);
+  if (e != hipSuccess) return hip_fail(e, "CS_DEBUG_CHECK metadata copy");
+  if (cu[0] != 0) return fail(CS_ERR_INVALID_ARG, "cu_q_lens[0] = %d, expected 0", cu[0]);
+  if (cu[batch] != total_q)
+    return fail(CS_ERR_INVALID_ARG, "cu_q_lens[batch] = %d but total_q = %d", cu[batch], total_q);
+  for (int r = 0; r < batch; ++r) {
+    const long long s = (long long)cu[r + 1] - cu[r];
+    if (s < 0) return fail(CS_ERR_INVALID_ARG, "cu_q_lens decreases at %d", r);
+    if (s > max_q_len) return fail(CS_ERR_INVALID_ARG, "S_%d = %lld exceeds max_q_len %d", r, s, max_q_len);
+    if (pl[r] < 0) return fail(CS_ERR_INVALID_ARG, "prefix_lens[%d] = %d is negative", r, pl[r]);
+    const long long len = s + pl[r];
+    if (len > max_kv_len)
+      return fail(CS_ERR_INVALID_ARG, "P_%d + S_%d = %lld exceeds max_kv_len %d", r, r, len, max_kv_len);
+    const long long nb = (len + 15) / 16;
+    for (long long b = 0; b < nb; ++b) {
+      const int32_t slot = bt[(size_t)r * max_blocks_per_seq + b];
+      if (slot < 0 || slot >= num_blocks)
+        return fail(CS_ERR_INVALID_ARG, "block_tables[%d][%lld] = %d outside [0, %d)", r, b, slot, num_blocks);
+    }
+  }
+  return CS_OK;
+}
+
+int debug_check_prefetch(const int32_t* dst, int n, int num_blocks, hipStream_t stream) {
+  std::vector<int32_t> ids;
+  hipError_t e = copy_to_host(ids, dst, (size_t)n, stream);
+  if (e != hipSuccess) return hip_fail(e, "CS_DEBUG_CHECK metadata copy");
+  std::vector<unsigned char> seen((size_t)num_blocks, 0);
+  for (int i = 0; i < n; ++i) {
+    if (ids[i] < 0 || ids[i] >= num_blocks)
+      return fail(CS_ERR_INVALID_ARG, "dst_block_ids[%d] = %d outside [0, %d)", i, ids[i], num_blocks);
+    if (seen[ids[i]]) return fail(CS_ERR_INVALID_ARG, "dst_block_ids[%d] = %d is a duplicate", i, ids[i]);
+    seen[ids[i]] = 1;
+  }
+  return CS_OK;
+}
+
+// Device-visible address of a pinned, device-mapped host buffer, or null.
+const void* mapped_host_pointer(const void* host, const char* name, int* status) {
+  hipPointerAttribute_t attr;
+  memset(&attr, 0, sizeof(attr));
+  hipError_t e = hipPointerGetAttributes(&attr, host);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();   // clear the sticky error of the failed query
+    *status = fail(CS_ERR_INVALID_ARG, "%s is not pinned host memory (%s)", name, hipGetErrorString(e));
+    return nullptr;
+  }
+  if (attr.type != hipMemoryTypeHost || attr.devicePointer == nullptr || attr.hostPointer == nullptr) {
+    *status = fail(CS_ERR_INVALID_ARG, "%s is not pinned, device-mapped host memory", name);
+    return nullptr;
+  }
+  const char* base_h = static_cast<const char*>(attr.hostPointer);
+  const char* base_d = static_cast<const char*>(attr.devicePointer);
+  *status = CS_OK;
+  return base_d + (static_cast<const char*>(host) - base_h);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* cs_status_string(int status) {
+  switch (status) {
+    case CS_OK: return "CS_OK";
+    case CS_ERR_INVALID_ARG: return "CS_ERR_INVALID_ARG";
+    case CS_ERR_UNSUPPORTED: return "CS_ERR_UNSUPPORTED";
+    case CS_ERR_HIP: return "CS_ERR_HIP";
+    default: return "CS_UNKNOWN_STATUS";
+  }
+}
+
+const char* cs_last_error(void) { return g_last_error; }
+
+int cs_prefill_paged_attn(const void* q, const void* k_pool, const void* v_pool,
+                          const int32_t* block_tables, const int32_t* prefix_lens,
+                          const int32_t* cu_q_lens, int32_t batch, int32_t total_q,
+                          int32_t max_q_len, int32_t max_kv_len, int32_t max_blocks_per_seq,
+                          int32_t num_blocks, int32_t num_q_heads, int32_t num_kv_heads,
+                          int32_t head_dim, int32_t block_size, float scale, void* out,
+                          cs_stream_t stream) {
+  if (batch < 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0 || max_blocks_per_seq < 0 ||
+      num_blocks < 0)
+    return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+    return fail(CS_ERR_INVALID_ARG, "head counts, head_dim and block_size must be positive");
+  if (num_q_heads % num_kv_heads != 0)
+    return fail(CS_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                num_q_heads, num_kv_heads);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
+  if (!isfinite(scale)) return fail(CS_ERR_INVALID_ARG, "scale is not finite");
+  if (batch == 0 || total_q == 0 || max_q_len == 0) return ok();
+  if (!q || !k_pool || !v_pool || !block_tables || !prefix_lens || !cu_q_lens || !out)
+    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  if (num_blocks == 0) return fail(CS_ERR_INVALID_ARG, "num_blocks is 0");
+  if (max_q_len > max_kv_len) return fail(CS_ERR_INVALID_ARG, "max_q_len exceeds max_kv_len");
+  if ((long long)max_blocks_per_seq * block_size < max_kv_len)
+    return fail(CS_ERR_INVALID_ARG, "max_blocks_per_seq * block_size < max_kv_len");
+  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
+    return fail(CS_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be 16-byte aligned");
+  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, num_q_heads, num_kv_heads);
+  if (geo.grid > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (debug_checks_enabled()) {
+    int st = debug_check_attn(block_tables, prefix_lens, cu_q_lens, batch, total_q, max_q_len,
+                              max_kv_len, max_blocks_per_seq, num_blocks, s);
+    if (st != CS_OK) return st;
+  }
+  cs::AttnLaunch a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_tables = block_tables;
+  a.prefix_lens = prefix_lens;
+  a.cu_q_lens = cu_q_lens;
+  a.out = static_cast<uint16_t*>(out);
+  a.batch = batch;
+  a.max_q_len = max_q_len;
+  a.max_blocks_per_seq = max_blocks_per_seq;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.scale = scale;
+  hipError_t e = cs::launch_prefill_paged_attn(a, s);
+  if (e != hipSuccess) return hip_fail(e, "prefill_paged_attn launch");
+  return ok();
+}
+
+int cs_kv_prefetch(const void* host_k_blocks, const void* host_v_blocks,
+                   const int32_t* dst_block_ids, int32_t n, void* k_pool, void* v_pool,
+                   int32_t num_blocks, int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                   cs_stream_t stream) {
+  if (n < 0 || num_blocks < 0) return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+    return fail(CS_ERR_INVALID_ARG, "num_kv_heads, head_dim and block_size must be positive");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
+  if (n == 0) return ok();
+  if (!host_k_blocks || !host_v_blocks || !dst_block_ids || !k_pool || !v_pool)
+    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  if (n > num_blocks) return fail(CS_ERR_INVALID_ARG, "n = %d exceeds num_blocks = %d", n, num_blocks);
+  if (!aligned16(host_k_blocks) || !aligned16(host_v_blocks) || !aligned16(k_pool) ||
+      !aligned16(v_pool))
+    return fail(CS_ERR_INVALID_ARG, "host buffers and pools must be 16-byte aligned");
+  int st = CS_OK;
+  const void* dk = mapped_host_pointer(host_k_blocks, "host_k_blocks", &st);
+  if (st != CS_OK) return st;
+  const void* dv = mapped_host_pointer(host_v_blocks, "host_v_blocks", &st);
+  if (st != CS_OK) return st;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (debug_checks_enabled()) {
+    st = debug_check_prefetch(dst_block_ids, n, num_blocks, s);
+    if (st != CS_OK) return st;
+  }
+  cs::PrefetchLaunch a;
+  a.host_k = static_cast<const uint16_t*>(dk);
+  a.host_v = static_cast<const uint16_t*>(dv);
+  a.dst = dst_block_ids;
+  a.n = n;
+  a.k_pool = static_cast<uint16_t*>(k_pool);
+  a.v_pool = static_cast<uint16_t*>(v_pool);
+  a.block_bytes = (long long)num_kv_heads * block_size * head_dim * 2;
+  hipError_t e = cs::launch_kv_prefetch(a, s);
+  if (e != hipSuccess) return hip_fail(e, "kv_prefetch launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,51 @@
+// Internal declarations shared by the C ABI layer (api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cs {
+
+// Everything the attention kernel needs, already validated by the ABI layer.
+struct AttnLaunch {
+  const uint16_t* q;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_tables;
+  const int32_t* prefix_lens;
+  const int32_t* cu_q_lens;
+  uint16_t* out;
+  int batch;
+  int max_q_len;
+  int max_blocks_per_seq;
+  int num_q_heads;
+  int num_kv_heads;
+  int head_dim;
+  float scale;
+};
+
+// Launch geometry of the attention kernel (host-side, for tests and tuning).
+struct AttnGeometry {
+  int heads_per_wg;   // query heads of one GQA group handled by one work-group
+  int span;           // suffix tokens handled by one work-group
+  int token_tiles;    // span-sized token tiles per invocation (upper bound)
+  int head_tiles;     // num_q_heads / heads_per_wg
+  long long grid;     // work-groups launched
+};
+
+AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads);
+hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream);
+
+struct PrefetchLaunch {
+  const uint16_t* host_k;   // device-visible addresses of the pinned host buffers
+  const uint16_t* host_v;
+  const int32_t* dst;
+  int n;
+  uint16_t* k_pool;
+  uint16_t* v_pool;
+  long long block_bytes;    // num_kv_heads * block_size * head_dim * 2
+};
+
+hipError_t launch_kv_prefetch(const PrefetchLaunch& a, hipStream_t stream);
+
+}  // namespace cs

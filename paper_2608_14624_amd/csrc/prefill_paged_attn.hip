@@ -1,0 +1,313 @@
+// Paged prefix-reuse prefill attention for gfx950 (CDNA4).
+//
+// What it computes (arXiv 2608.14624, Sec. 2.1 "Prefix caching"): the suffix
+// queries of each agent invocation attend over the KV of the cached prefix
+// (the agent anchor) and of the suffix itself, all of it stored in 16-token
+// blocks of a paged pool and reached through the invocation's block table;
+// suffix row i is prompt position P + i and sees keys 0 .. P + i.
+//
+// Kernel design
+//   * One work-group = 4 wave64s = one (invocation, group of query heads that
+//     share one KV head, tile of suffix tokens).  Each wave owns 32 query rows
+//     (one head x 32 consecutive tokens), so every K/V tile staged in LDS is
+//     used by 4 waves: by 4 heads of the GQA group when the group has at
+//     least 4 heads, otherwise by consecutive token tiles of fewer heads.
+//   * The contractions run on bf16 MFMA (v_mfma_f32_32x32x16_bf16) in the
+//     transposed orientation S^T = K Q^T and O^T = V^T P^T.  In that
+//     orientation a lane owns one query: the row max and row sum of the
+//     online softmax are in-lane reductions plus one exchange between the two
+//     lane halves, and the probabilities leave the S^T accumulator already in
+//     the register layout of the B operand of the PV product.
+//   * Keys are consumed 64 at a time (4 pool blocks).  K is staged row-major
+//     [key][d]; V is staged transposed [d][key] so that the A operand of the
+//     PV product is two 8-byte LDS reads.  Rows are padded to spread LDS
+//     banks.  Block ids are read from the block table per 16-token block.
+//   * Masking is a select to -inf (never an additive mask), so positions past
+//     the end of a sequence inside its last block never contribute whatever
+//     they hold; whole blocks past the end are zero-filled in LDS, never read.
+//   * Softmax runs in base 2 with log2(e) folded into the scale.
+//
+// Work-group order: the head-tile index varies fastest, so with 8 head tiles
+// the 8 XCDs each serve one KV head and its K/V stays in that XCD's L2; token
+// tiles are issued from the last (most keys) to the first.
+#include "internal.h"
+
+#include <math.h>
+
+namespace cs {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kBlock = 16;    // tokens per pool block
+constexpr int kBN = 64;       // keys per step
+constexpr int kNQ = 32;       // query rows per wave
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr float kLog2e = 1.4426950408889634f;
+
+struct Params {
+  const uint16_t* q;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_tables;
+  const int32_t* prefix_lens;
+  const int32_t* cu_q_lens;
+  uint16_t* out;
+  int batch;
+  int max_blocks_per_seq;
+  int num_q_heads;
+  int num_kv_heads;
+  int group;          // query heads per KV head
+  int heads_per_wg;
+  int span;
+  int token_tiles;
+  int head_tiles;
+  float scale_log2;   // scale * log2(e)
+};
+
+template <int D>
+struct Lds {
+  static constexpr int kStride = D + 8;       // K rows: [key][d], 16 B pad
+  static constexpr int vStride = kBN + 4;     // V^T rows: [d][key], 8 B pad
+  uint16_t k[kBN * kStride];
+  uint16_t vt[D * vStride];
+};
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) {
+  __shared__ Lds<D> sm;
+  constexpr int kStride = Lds<D>::kStride;
+  constexpr int vStride = Lds<D>::vStride;
+  constexpr int KS = D / 16;     // MFMA k-steps over the head dim
+  constexpr int DT = D / 32;     // 32-wide output tiles over the head dim
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int qi = lane & 31;
+  const int half = lane >> 5;
+
+  // ---- work tile -----------------------------------------------------
+  const int wg = blockIdx.x;
+  const int head_tile = wg % p.head_tiles;
+  const int rest = wg / p.head_tiles;
+  const int r = rest % p.batch;
+  const int token_tile = p.token_tiles - 1 - rest / p.batch;
+  const int q0 = p.cu_q_lens[r];
+  const int S = p.cu_q_lens[r + 1] - q0;
+  const int t0 = token_tile * p.span;
+  if (t0 >= S) return;
+  const int P = p.prefix_lens[r];
+  const int L = P + S;
+
+  const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
+  const int g = h / p.group;
+  const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
+  const bool row_valid = t < S;
+  const int qpos = row_valid ? P + t : L - 1;              // last visible key
+  const int kv_end = P + min(S, t0 + p.span);              // keys the tile needs
+  const int n_steps = (kv_end + kBN - 1) / kBN;
+  const int n_blk = (L + kBlock - 1) / kBlock;
+  const int32_t* bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
+  const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
+  const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
+  const uint16_t* kbase = p.k_pool + (size_t)g * tile_elems;
+  const uint16_t* vbase = p.v_pool + (size_t)g * tile_elems;
+
+  // ---- Q^T operand: lane holds query qi, dims ks*16 + half*8 .. +7 -----
+  const size_t qrow = ((size_t)(q0 + t) * p.num_q_heads + h) * D;
+  bf16x8 qreg[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (row_valid) v = *reinterpret_cast<const uint4*>(p.q + qrow + ks * 16 + half * 8);
+    qreg[ks] = as_bf16x8(v);
+  }
+
+  f32x16 oacc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+  float m_run = -INFINITY;
+  float l_run = 0.f;
+
+  for (int step = 0; step < n_steps; ++step) {
+    const int kstart = step * kBN;
+    __syncthreads();   // previous step's LDS reads are done
+
+    // ---- stage K [key][d] ------------------------------------------
+    constexpr int kChunksPerRow = D / 8;
+    constexpr int kChunks = kBN * kChunksPerRow;
+#pragma unroll
+    for (int c = tid; c < kChunks; c += kThreads) {
+      const int key = c / kChunksPerRow;
+      const int dc = c % kChunksPerRow;
+      const int j = kstart + key;
+      const int lb = j / kBlock;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (lb < n_blk) {
+        const size_t slot = (size_t)bt[lb];
+        v = *reinterpret_cast<const uint4*>(kbase + slot * slot_elems + (j % kBlock) * D + dc * 8);
+      }
+      *reinterpret_cast<uint4*>(&sm.k[key * kStride + dc * 8]) = v;
+    }
+    // ---- stage V^T [d][key]: each item moves 4 keys x 8 dims --------
+    constexpr int kItems = (kBN / 4) * kChunksPerRow;
+#pragma unroll
+    for (int c = tid; c < kItems; c += kThreads) {
+      const int quad = c / kChunksPerRow;
+      const int dc = c % kChunksPerRow;
+      const int j0 = kstart + quad * 4;        // 4 keys inside one block
+      const int lb = j0 / kBlock;
+      uint4 v[4] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0),
+                    make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
+      if (lb < n_blk) {
+        const size_t slot = (size_t)bt[lb];
+        const uint16_t* src = vbase + slot * slot_elems + (j0 % kBlock) * D + dc * 8;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(src + u * D);
+      }
+      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&v[0]);
+      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&v[1]);
+      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&v[2]);
+      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&v[3]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int sh = (e & 1) * 16;
+        const uint32_t a0 = (w0[e >> 1] >> sh) & 0xffffu;
+        const uint32_t a1 = (w1[e >> 1] >> sh) & 0xffffu;
+        const uint32_t a2 = (w2[e >> 1] >> sh) & 0xffffu;
+        const uint32_t a3 = (w3[e >> 1] >> sh) & 0xffffu;
+        uint2 packed = make_uint2(a0 | (a1 << 16), a2 | (a3 << 16));
+        *reinterpret_cast<uint2*>(&sm.vt[(dc * 8 + e) * vStride + quad * 4]) = packed;
+      }
+    }
+    __syncthreads();
+
+    // ---- S^T = K Q^T: two 32-key tiles ------------------------------
+    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const uint4 a = *reinterpret_cast<const uint4*>(&sm.k[(mt * 32 + qi) * kStride + ks * 16 + half * 8]);
+        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], sacc[mt], 0, 0, 0);
+      }
+    }
+
+    // ---- mask, running max ------------------------------------------
+    // accumulator register rr of tile mt holds key
+    //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
+        float s = sacc[mt][rr] * p.scale_log2;
+        s = (kj <= qpos) ? s : -INFINITY;
+        sacc[mt][rr] = s;
+        mloc = fmaxf(mloc, s);
+      }
+    }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float m_new = fmaxf(m_run, mloc);     // finite: key 0 is visible to every row
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) {
+        const float e = __builtin_amdgcn_exp2f(sacc[mt][rr] - m_new);
+        sacc[mt][rr] = e;
+        l_run += e;
+      }
+    }
+
+    // ---- O^T += V^T P^T: four 16-key MFMA steps --------------------
+#pragma unroll
+    for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
+      const int mt = ks2 >> 1;
+      const int rb = (ks2 & 1) * 8;
+      bf16x8 b;
+#pragma unroll
+      for (int s = 0; s < 8; ++s) b[s] = (__bf16)sacc[mt][rb + s];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const uint16_t* vrow = &sm.vt[(dt * 32 + qi) * vStride + ks2 * 16 + 4 * half];
+        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
+        const uint4 a = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), b, oacc[dt], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- epilogue: O / l, bf16, store --------------------------------
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float inv = 1.f / l_tot;
+  if (row_valid) {
+    uint16_t* orow = p.out + qrow;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        bf16x4 o;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) o[u] = (__bf16)(oacc[dt][rg * 4 + u] * inv);
+        *reinterpret_cast<uint2*>(orow + dt * 32 + 8 * rg + 4 * half) = __builtin_bit_cast(uint2, o);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads) {
+  AttnGeometry geo;
+  const int group = num_q_heads / num_kv_heads;
+  geo.heads_per_wg = (group % 4 == 0) ? 4 : (group % 2 == 0) ? 2 : 1;
+  geo.span = kNQ * (kWaves / geo.heads_per_wg);
+  geo.token_tiles = (max_q_len + geo.span - 1) / geo.span;
+  geo.head_tiles = num_q_heads / geo.heads_per_wg;
+  geo.grid = (long long)geo.token_tiles * batch * geo.head_tiles;
+  return geo;
+}
+
+hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
+  const AttnGeometry geo = attn_geometry(a.batch, a.max_q_len, a.num_q_heads, a.num_kv_heads);
+  Params p;
+  p.q = a.q;
+  p.k_pool = a.k_pool;
+  p.v_pool = a.v_pool;
+  p.block_tables = a.block_tables;
+  p.prefix_lens = a.prefix_lens;
+  p.cu_q_lens = a.cu_q_lens;
+  p.out = a.out;
+  p.batch = a.batch;
+  p.max_blocks_per_seq = a.max_blocks_per_seq;
+  p.num_q_heads = a.num_q_heads;
+  p.num_kv_heads = a.num_kv_heads;
+  p.group = a.num_q_heads / a.num_kv_heads;
+  p.heads_per_wg = geo.heads_per_wg;
+  p.span = geo.span;
+  p.token_tiles = geo.token_tiles;
+  p.head_tiles = geo.head_tiles;
+  p.scale_log2 = a.scale * kLog2e;
+  const dim3 grid((unsigned)geo.grid), block(kThreads);
+  if (a.head_dim == 128) {
+    hipLaunchKernelGGL(prefill_paged_attn_kernel<128>, grid, block, 0, stream, p);
+  } else {
+    hipLaunchKernelGGL(prefill_paged_attn_kernel<64>, grid, block, 0, stream, p);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace cs

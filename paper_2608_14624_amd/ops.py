@@ -1,0 +1,168 @@
+"""Python binding of libcachescout.so (argument marshalling only).
+
+The functions keep the C names.  They take PyTorch tensors for device memory,
+pinned host memory and streams, pass raw pointers and sizes to the C ABI and
+raise :class:`CacheScoutError` on a non-zero status.  All computation happens
+in the HIP kernels; there is no fallback path: if the shared library is
+missing or fails to load, importing this module raises.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcachescout.so")
+
+CS_OK = 0
+CS_ERR_INVALID_ARG = 1
+CS_ERR_UNSUPPORTED = 2
+CS_ERR_HIP = 3
+
+# every symbol the C header declares
+EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_status_string", "cs_last_error")
+
+
+class CacheScoutError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{status_string(status)}: {message}")
+        self.status = status
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(
+            f"{_LIB_PATH} is missing: build it with `python -m paper_2608_14624_amd.build` "
+            "(or __graft_entry__.build()); there is no non-HIP fallback")
+    lib = ctypes.CDLL(_LIB_PATH)
+    i32, vp, f32 = ctypes.c_int32, ctypes.c_void_p, ctypes.c_float
+    lib.cs_prefill_paged_attn.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                                          i32, i32, i32, i32, f32, vp, vp]
+    lib.cs_prefill_paged_attn.restype = ctypes.c_int
+    lib.cs_kv_prefetch.argtypes = [vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp]
+    lib.cs_kv_prefetch.restype = ctypes.c_int
+    lib.cs_status_string.argtypes = [ctypes.c_int]
+    lib.cs_status_string.restype = ctypes.c_char_p
+    lib.cs_last_error.argtypes = []
+    lib.cs_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+_lib = _load()
+LIB_PATH = _LIB_PATH
+
+
+def status_string(status):
+    return _lib.cs_status_string(int(status)).decode()
+
+
+def last_error():
+    return _lib.cs_last_error().decode()
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream_handle(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status):
+    if status != CS_OK:
+        raise CacheScoutError(status, last_error())
+
+
+def cs_prefill_paged_attn_raw(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, batch,
+                              total_q, max_q_len, max_kv_len, max_blocks_per_seq, num_blocks,
+                              num_q_heads, num_kv_heads, head_dim, block_size, scale, out,
+                              stream=0):
+    """The C call with raw pointers (ints or None); returns the status code."""
+    return _lib.cs_prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens,
+                                      batch, total_q, max_q_len, max_kv_len, max_blocks_per_seq,
+                                      num_blocks, num_q_heads, num_kv_heads, head_dim,
+                                      block_size, ctypes.c_float(scale), out, stream)
+
+
+def cs_kv_prefetch_raw(host_k, host_v, dst_block_ids, n, k_pool, v_pool, num_blocks,
+                       num_kv_heads, head_dim, block_size, stream=0):
+    """The C call with raw pointers (ints or None); returns the status code."""
+    return _lib.cs_kv_prefetch(host_k, host_v, dst_block_ids, n, k_pool, v_pool, num_blocks,
+                               num_kv_heads, head_dim, block_size, stream)
+
+
+def _require(cond, msg):
+    if not cond:
+        raise CacheScoutError(CS_ERR_INVALID_ARG, msg)
+
+
+def cs_prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out, *,
+                          max_q_len, max_kv_len, scale, stream=None):
+    """Enqueue paged prefill attention on ``stream`` (default: the current stream).
+
+    Tensors: ``q``/``out`` bf16 ``[total_q, Hq, D]``; pools bf16
+    ``[num_blocks, Hkv, 16, D]``; ``block_tables`` int32 ``[B, max_blocks]``;
+    ``prefix_lens`` int32 ``[B]``; ``cu_q_lens`` int32 ``[B+1]``; all on the
+    same GPU and contiguous.  ``max_q_len``/``max_kv_len`` are host integers
+    bounding the suffix and total lengths.
+    """
+    dev = q.device
+    for name, t, dt in (("q", q, torch.bfloat16), ("k_pool", k_pool, torch.bfloat16),
+                        ("v_pool", v_pool, torch.bfloat16), ("out", out, torch.bfloat16),
+                        ("block_tables", block_tables, torch.int32),
+                        ("prefix_lens", prefix_lens, torch.int32),
+                        ("cu_q_lens", cu_q_lens, torch.int32)):
+        _require(t.device == dev and t.is_cuda, f"{name} must be on {dev}")
+        _require(t.dtype == dt, f"{name} must be {dt}")
+        _require(t.is_contiguous(), f"{name} must be contiguous")
+    _require(q.dim() == 3 and out.shape == q.shape, "q and out must be [total_q, Hq, D]")
+    _require(k_pool.dim() == 4 and v_pool.shape == k_pool.shape,
+             "pools must be [num_blocks, Hkv, block_size, D]")
+    _require(block_tables.dim() == 2, "block_tables must be [B, max_blocks]")
+    total_q, hq, d = q.shape
+    num_blocks, hkv, bs, d2 = k_pool.shape
+    _require(d == d2, "head_dim of q and pools differ")
+    batch = block_tables.shape[0]
+    _require(prefix_lens.numel() == batch and cu_q_lens.numel() == batch + 1,
+             "prefix_lens must have B entries and cu_q_lens B + 1")
+    status = cs_prefill_paged_attn_raw(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_tables), _ptr(prefix_lens),
+        _ptr(cu_q_lens), batch, total_q, int(max_q_len), int(max_kv_len),
+        block_tables.shape[1], num_blocks, hq, hkv, d, bs, float(scale), _ptr(out),
+        _stream_handle(stream, dev))
+    _check(status)
+
+
+def cs_kv_prefetch(host_k, host_v, dst_block_ids, k_pool, v_pool, *, stream=None):
+    """Enqueue the host-to-pool block copy on ``stream`` (default: current stream).
+
+    ``host_k``/``host_v``: pinned CPU bf16 tensors ``[n, Hkv, 16, D]``;
+    ``dst_block_ids``: int32 GPU tensor ``[n]``; pools as for attention.
+    """
+    dev = k_pool.device
+    _require(host_k.device.type == "cpu" and host_v.device.type == "cpu",
+             "host blocks must be CPU tensors")
+    _require(host_k.is_pinned() and host_v.is_pinned(), "host blocks must be pinned")
+    _require(host_k.dtype == torch.bfloat16 and host_v.dtype == torch.bfloat16,
+             "host blocks must be bf16")
+    _require(host_k.is_contiguous() and host_v.is_contiguous(), "host blocks must be contiguous")
+    _require(dst_block_ids.dtype == torch.int32 and dst_block_ids.device == dev,
+             "dst_block_ids must be int32 on the pool's device")
+    _require(k_pool.shape == v_pool.shape and k_pool.dtype == torch.bfloat16,
+             "pools must match and be bf16")
+    n = dst_block_ids.numel()
+    _require(host_k.shape[0] >= n and host_v.shape[0] >= n, "fewer host blocks than ids")
+    _require(tuple(host_k.shape[1:]) == tuple(k_pool.shape[1:]), "host block shape != pool block shape")
+    num_blocks, hkv, bs, d = k_pool.shape
+    status = cs_kv_prefetch_raw(_ptr(host_k), _ptr(host_v), _ptr(dst_block_ids), n,
+                                _ptr(k_pool), _ptr(v_pool), num_blocks, hkv, d, bs,
+                                _stream_handle(stream, dev))
+    _check(status)

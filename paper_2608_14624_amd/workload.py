@@ -19,10 +19,15 @@ Shapes follow the paper's setting (arXiv 2608.14624):
 * the predicted next agent's anchor blocks may sit in the CPU tier and are
   reloaded into free pool slots before use (Sec. 3.4, Sec. 4).
 
-Values are N(0, 1) float32 draws rounded to nearest-even bf16 and stored as
-uint16 bit patterns.  Every random stream is keyed by ``(seed, kind, index)``
-so that an agent's anchor content does not depend on how many invocations
-were drawn before it.
+Values are N(0, 1) in bf16, stored as uint16 bit patterns, drawn by inverse
+transform sampling: a uniform 16-bit integer ``u`` selects the bf16 value
+(nearest-even) of the standard normal quantile at ``(u + 0.5) / 65536``.
+bf16 itself has only 65536 codes, so this is a faithful N(0, 1) at bf16
+resolution (tails clipped at +/-4.31), and about six times faster than
+rounding float32 normal draws, which matters for the 3 GB configurations.
+Every random stream is keyed by ``(seed, kind, index)`` so that an agent's
+anchor content does not depend on how many invocations were drawn before
+it.
 
 Pool conventions:
 
@@ -61,8 +66,28 @@ def f32_to_bf16_bits(x):
     return ((u + bias) >> np.uint32(16)).astype(np.uint16)
 
 
+_NORMAL_TABLE = None
+
+
+def normal_bf16_table():
+    """bf16 codes of the N(0, 1) quantiles at the midpoints of 65536 equal bins."""
+    global _NORMAL_TABLE
+    if _NORMAL_TABLE is None:
+        from scipy.special import ndtri
+        mid = (np.arange(65536, dtype=np.float64) + 0.5) / 65536.0
+        _NORMAL_TABLE = f32_to_bf16_bits(ndtri(mid).astype(np.float32))
+    return _NORMAL_TABLE
+
+
 def _normal_bf16(rng, shape):
-    return f32_to_bf16_bits(rng.standard_normal(size=shape, dtype=np.float32))
+    n = int(np.prod(shape))
+    codes = rng.integers(0, 65536, size=n, dtype=np.uint16)
+    out = np.empty(n, dtype=np.uint16)
+    table = normal_bf16_table()
+    step = 1 << 20        # bounded index temporaries
+    for a in range(0, n, step):
+        np.take(table, codes[a:a + step], out=out[a:a + step])
+    return out.reshape(shape)
 
 
 @dataclass
@@ -295,14 +320,16 @@ def build_workload(name, seed, anchor_lens, invocations, num_q_heads, num_kv_hea
         k_pool[agent_slots[a][resident]] = kb[resident]
         v_pool[agent_slots[a][resident]] = vb[resident]
 
-    # per-invocation private blocks and queries
-    q_parts = []
+    # per-invocation private blocks and queries, written in place
+    anchor_q = {}
+    cu_all = wl.cu_q_lens.astype(np.int64)
+    q_all = np.empty((int(cu_all[-1]), hq, d), dtype=np.uint16)
     for r, inv in enumerate(invs):
         sq, sk, sv = _suffix_content(wl, inv)
-        if inv.agent in anchors:
-            ak, av = anchors[inv.agent]
-        else:
+        if inv.agent not in anchors:
             ak, av, _ = _anchor_content(wl, inv.agent, need_q=False)
+            anchors[inv.agent] = (ak, av)
+        ak, av = anchors[inv.agent]
         f = private_from[r]
         n = n_blocks_seq[r]
         kk = np.concatenate([ak[f * bs:], sk], axis=0)
@@ -312,14 +339,17 @@ def build_workload(name, seed, anchor_lens, invocations, num_q_heads, num_kv_hea
         if f:
             block_tables[r, :f] = agent_slots[inv.agent]
         block_tables[r, f:n] = inv_slots[r]
+        c0, c1 = int(cu_all[r]), int(cu_all[r + 1])
         if inv.hit:
-            q_parts.append(sq)
+            q_all[c0:c1] = sq
         else:
-            rq = np.random.default_rng([seed, _K_ANCHOR_Q, inv.agent])
-            aq = _normal_bf16(rq, (anchor_lens[inv.agent], hq, d))
-            q_parts.append(np.concatenate([aq, sq], axis=0))
-    if q_parts:
-        wl.q = np.ascontiguousarray(np.concatenate(q_parts, axis=0))
+            if inv.agent not in anchor_q:
+                rq = np.random.default_rng([seed, _K_ANCHOR_Q, inv.agent])
+                anchor_q[inv.agent] = _normal_bf16(rq, (anchor_lens[inv.agent], hq, d))
+            pa = anchor_lens[inv.agent]
+            q_all[c0:c0 + pa] = anchor_q[inv.agent]
+            q_all[c0 + pa:c1] = sq
+    wl.q = q_all
     wl.q_gain = float(q_gain)
     wl.q = _apply_gain(wl.q, wl.q_gain)
     if off_dst:

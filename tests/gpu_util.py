@@ -1,0 +1,55 @@
+"""Helpers for the GPU tests: tolerances, sampling and comparison against the oracle."""
+
+import numpy as np
+
+import oracle
+
+# float tolerance on bf16 outputs against the unrounded float64 oracle
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+
+
+def bits_to_f64(bits):
+    return oracle.bf16_bits_to_f64(bits)
+
+
+def compare_full(got_bits, ref):
+    """Max-abs / mean-abs error of a full bf16 output against the float64 oracle."""
+    got = bits_to_f64(got_bits)
+    assert got.shape == ref.shape
+    assert np.isfinite(got).all(), "non-finite output"
+    err = np.abs(got - ref)
+    return float(err.max()), float(err.mean())
+
+
+def sample_rows(wl, n_random, seed, edge=True):
+    """(r, h, i) triples: random rows plus, per invocation, its first and last
+    rows and the rows around block and 32-row tile boundaries."""
+    rng = np.random.default_rng(seed)
+    q_lens = wl.q_lens
+    out = set()
+    nonempty = [r for r in range(wl.batch) if q_lens[r] > 0]
+    for _ in range(n_random):
+        r = int(rng.choice(nonempty))
+        out.add((r, int(rng.integers(wl.num_q_heads)), int(rng.integers(q_lens[r]))))
+    if edge:
+        for r in nonempty:
+            s = int(q_lens[r])
+            for i in {0, 1, 15, 16, 31, 32, 63, 64, s // 2, s - 2, s - 1}:
+                if 0 <= i < s:
+                    out.add((r, int(rng.integers(wl.num_q_heads)), i))
+    return sorted(out)
+
+
+def compare_rows(wl, got_bits, samples, k_pool=None, v_pool=None):
+    """Errors of sampled output rows against the oracle computed row by row."""
+    kp = wl.k_pool if k_pool is None else k_pool
+    vp = wl.v_pool if v_pool is None else v_pool
+    ref = oracle.prefill_paged_attn_rows(wl.q, kp, vp, wl.block_tables,
+                                         wl.prefix_lens, wl.cu_q_lens, wl.num_q_heads,
+                                         wl.num_kv_heads, wl.scale, samples)
+    cu = wl.cu_q_lens
+    got = np.stack([bits_to_f64(got_bits[int(cu[r]) + i, h]) for r, h, i in samples])
+    assert np.isfinite(got).all(), "non-finite output"
+    err = np.abs(got - ref)
+    return float(err.max()), float(err.mean())

@@ -1,0 +1,114 @@
+"""The C ABI library on the CPU: it loads, exports every declared symbol, and
+its host-side validation rejects bad arguments before touching a GPU.
+
+No kernel is launched here; every call below returns from the argument checks
+(or is a documented no-op) before the first HIP runtime call.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cachescout.h")
+
+ops = pytest.importorskip("paper_2608_14624_amd.ops",
+                          reason="libcachescout.so not built (run __graft_entry__.build())")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cs_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_expected_calls():
+    assert declared_functions() == sorted(ops.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(ops.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} not exported"
+
+
+def test_status_strings():
+    assert ops.status_string(0) == "CS_OK"
+    assert ops.status_string(1) == "CS_ERR_INVALID_ARG"
+    assert ops.status_string(2) == "CS_ERR_UNSUPPORTED"
+    assert ops.status_string(3) == "CS_ERR_HIP"
+    assert ops.status_string(77) == "CS_UNKNOWN_STATUS"
+
+
+FAKE = 1 << 20   # a 16-byte aligned non-null address; never dereferenced here
+
+GOOD = dict(q=FAKE, k_pool=FAKE, v_pool=FAKE, block_tables=FAKE, prefix_lens=FAKE,
+            cu_q_lens=FAKE, batch=2, total_q=10, max_q_len=8, max_kv_len=40,
+            max_blocks_per_seq=3, num_blocks=64, num_q_heads=8, num_kv_heads=2, head_dim=64,
+            block_size=16, scale=0.125, out=FAKE, stream=0)
+
+
+def attn(**kw):
+    args = dict(GOOD)
+    args.update(kw)
+    return ops.cs_prefill_paged_attn_raw(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(total_q=-5), ops.CS_ERR_INVALID_ARG),
+    (dict(num_kv_heads=3), ops.CS_ERR_INVALID_ARG),
+    (dict(num_q_heads=0), ops.CS_ERR_INVALID_ARG),
+    (dict(head_dim=96), ops.CS_ERR_UNSUPPORTED),
+    (dict(head_dim=256), ops.CS_ERR_UNSUPPORTED),
+    (dict(block_size=32), ops.CS_ERR_UNSUPPORTED),
+    (dict(scale=float("nan")), ops.CS_ERR_INVALID_ARG),
+    (dict(q=None), ops.CS_ERR_INVALID_ARG),
+    (dict(out=None), ops.CS_ERR_INVALID_ARG),
+    (dict(block_tables=None), ops.CS_ERR_INVALID_ARG),
+    (dict(max_blocks_per_seq=2), ops.CS_ERR_INVALID_ARG),    # 2 * 16 < 40
+    (dict(max_q_len=41), ops.CS_ERR_INVALID_ARG),
+    (dict(num_blocks=0), ops.CS_ERR_INVALID_ARG),
+    (dict(q=FAKE + 2), ops.CS_ERR_INVALID_ARG),               # misaligned
+    (dict(k_pool=FAKE + 8), ops.CS_ERR_INVALID_ARG),
+])
+def test_attention_rejects_bad_arguments(kw, status):
+    assert attn(**kw) == status
+    assert ops.last_error() != ""
+
+
+@pytest.mark.parametrize("kw", [dict(batch=0), dict(total_q=0), dict(max_q_len=0),
+                                dict(batch=0, q=None, out=None)])
+def test_attention_empty_work_is_a_noop(kw):
+    assert attn(**kw) == ops.CS_OK
+    assert ops.last_error() == ""
+
+
+PGOOD = dict(host_k=FAKE, host_v=FAKE, dst_block_ids=FAKE, n=4, k_pool=FAKE, v_pool=FAKE,
+             num_blocks=64, num_kv_heads=2, head_dim=64, block_size=16, stream=0)
+
+
+def prefetch(**kw):
+    args = dict(PGOOD)
+    args.update(kw)
+    return ops.cs_kv_prefetch_raw(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(head_dim=80), ops.CS_ERR_UNSUPPORTED),
+    (dict(block_size=8), ops.CS_ERR_UNSUPPORTED),
+    (dict(num_kv_heads=0), ops.CS_ERR_INVALID_ARG),
+    (dict(host_k=None), ops.CS_ERR_INVALID_ARG),
+    (dict(dst_block_ids=None), ops.CS_ERR_INVALID_ARG),
+    (dict(n=65), ops.CS_ERR_INVALID_ARG),
+    (dict(host_v=FAKE + 4), ops.CS_ERR_INVALID_ARG),
+])
+def test_prefetch_rejects_bad_arguments(kw, status):
+    assert prefetch(**kw) == status
+
+
+def test_prefetch_zero_blocks_is_a_noop():
+    assert prefetch(n=0, host_k=None, host_v=None) == ops.CS_OK

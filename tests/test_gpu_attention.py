@@ -1,0 +1,217 @@
+"""GPU parity of cs_prefill_paged_attn against the float64 oracle.
+
+Tolerance (bf16 output vs unrounded float64 oracle): max-abs <= 2e-2 and
+mean-abs <= 2e-3 over the compared elements.  Small and edge-case workloads
+are compared element by element; the full-size configurations are compared on
+sampled rows (random rows plus every invocation's first/last rows and rows at
+block and tile boundaries), with the launch configuration the benchmark uses.
+"""
+
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import MAX_ABS, MEAN_ABS, compare_full, compare_rows, sample_rows
+from paper_2608_14624_amd.workload import Invocation, build_workload, make_config
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def P():
+    from paper_2608_14624_amd import ops, pipeline
+    return ops, pipeline
+
+
+def run_full(P, wl):
+    _, pipeline = P
+    dw = pipeline.DeviceWorkload(wl)
+    dw.prefetch_all()
+    dw.attention()
+    torch.cuda.synchronize()
+    return dw
+
+
+def oracle_full(wl):
+    kp, vp = wl.k_pool, wl.v_pool
+    if wl.prefetch_dst is not None:
+        kp, vp = oracle.kv_prefetch(wl.host_k, wl.host_v, wl.prefetch_dst, kp, vp)
+    return oracle.prefill_paged_attn(wl.q, kp, vp, wl.block_tables, wl.prefix_lens,
+                                     wl.cu_q_lens, wl.num_q_heads, wl.num_kv_heads, wl.scale)
+
+
+def check_full(P, wl):
+    print(f"[case] {wl.name}: B={wl.batch} total_q={wl.total_q} Hq={wl.num_q_heads} "
+          f"Hkv={wl.num_kv_heads} D={wl.head_dim}", flush=True)
+    dw = run_full(P, wl)
+    mx, mean = compare_full(dw.out_bits(), oracle_full(wl))
+    print(f"    max_abs={mx:.3e} mean_abs={mean:.3e}", flush=True)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+    return dw
+
+
+def test_tiny_full(P):
+    check_full(P, make_config("tiny"))
+
+
+def test_llama8b_full(P):
+    check_full(P, make_config("llama8b"))
+
+
+EDGE = {
+    # name: (anchor_lens, invocations, Hq, Hkv, D, extra)
+    "single_token_suffix": ([100], [Invocation(0, 1)], 8, 2, 128, {}),
+    "prefix_not_block_multiple": ([37, 5], [Invocation(0, 50), Invocation(1, 17)], 8, 2, 128, {}),
+    "miss_and_hit_mix": ([70], [Invocation(0, 40), Invocation(0, 33, hit=False), Invocation(0, 1)], 8, 8, 64, {}),
+    "empty_suffix_in_batch": ([48, 20], [Invocation(0, 0), Invocation(1, 70), Invocation(0, 0), Invocation(1, 3)], 4, 1, 128, {}),
+    "group1_mha": ([64], [Invocation(0, 129)], 4, 4, 64, {}),
+    "group2": ([33], [Invocation(0, 97)], 4, 2, 128, {}),
+    "group8": ([200], [Invocation(0, 65), Invocation(0, 31)], 16, 2, 128, {}),
+    "group3": ([17], [Invocation(0, 45)], 6, 2, 64, {}),
+    "zero_prefix_hit": ([0], [Invocation(0, 77)], 8, 2, 128, {}),
+    "peaky_logits": ([90], [Invocation(0, 70)], 8, 2, 128, {"q_gain": 8.0}),
+    "long_ragged_tile": ([1000], [Invocation(0, 257), Invocation(0, 129)], 32, 8, 128, {}),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_edge_cases_full(P, name):
+    anchors, invs, hq, hkv, d, extra = EDGE[name]
+    wl = build_workload(name, 1234, anchors, invs, num_q_heads=hq, num_kv_heads=hkv,
+                        head_dim=d, num_blocks=256, **extra)
+    check_full(P, wl)
+
+
+def test_agent_batch_sampled(P):
+    _, pipeline = P
+    wl = make_config("agent_batch")
+    print(f"[case] agent_batch total_q={wl.total_q}", flush=True)
+    dw = pipeline.DeviceWorkload(wl)
+    dw.attention()
+    torch.cuda.synchronize()
+    samples = sample_rows(wl, 600, seed=2)
+    mx, mean = compare_rows(wl, dw.out_bits(), samples)
+    print(f"    {len(samples)} rows: max_abs={mx:.3e} mean_abs={mean:.3e}", flush=True)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
+def test_llama70b_prefetch_pipeline_sampled(P):
+    """The benchmark's launch configuration: per-agent attention with the next
+    agent's CPU-tier blocks prefetched on a side stream."""
+    _, pipeline = P
+    wl = make_config("llama70b_prefetch")
+    print(f"[case] llama70b_prefetch pipeline total_q={wl.total_q}", flush=True)
+    dw = pipeline.DeviceWorkload(wl)
+    pipe = pipeline.AgentPipeline(dw)
+    pipe.stage_first()
+    dw.out.fill_(float("nan"))
+    pipe.step()
+    torch.cuda.synchronize()
+    kp, vp = oracle.kv_prefetch(wl.host_k, wl.host_v, wl.prefetch_dst, wl.k_pool, wl.v_pool)
+    samples = sample_rows(wl, 400, seed=3)
+    mx, mean = compare_rows(wl, dw.out_bits(), samples, kp, vp)
+    print(f"    {len(samples)} rows: max_abs={mx:.3e} mean_abs={mean:.3e}", flush=True)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+    # the pools on the device now equal the oracle's post-prefetch pools
+    assert np.array_equal(dw.k_pool.view(torch.int16).cpu().numpy().view(np.uint16), kp)
+    assert np.array_equal(dw.v_pool.view(torch.int16).cpu().numpy().view(np.uint16), vp)
+    # every output row was written
+    assert torch.isfinite(dw.out.float()).all().item()
+
+
+@pytest.mark.slow
+def test_long_mixed_sampled(P):
+    _, pipeline = P
+    wl = make_config("long_mixed")
+    print(f"[case] long_mixed total_q={wl.total_q}", flush=True)
+    dw = pipeline.DeviceWorkload(wl)
+    dw.attention()
+    torch.cuda.synchronize()
+    samples = sample_rows(wl, 300, seed=4)
+    mx, mean = compare_rows(wl, dw.out_bits(), samples)
+    print(f"    {len(samples)} rows: max_abs={mx:.3e} mean_abs={mean:.3e}", flush=True)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
+def small_batch():
+    invs = [Invocation(0, 40), Invocation(1, 90), Invocation(0, 7), Invocation(2, 33, hit=False)]
+    return build_workload("inv", 77, [61, 128, 30], invs, num_q_heads=8, num_kv_heads=2,
+                          head_dim=128, num_blocks=128)
+
+
+def test_block_permutation_is_bitwise_invariant(P):
+    wl = small_batch()
+    base = run_full(P, wl).out_bits()
+    perm = np.random.default_rng(5).permutation(wl.num_blocks)
+    k2 = np.empty_like(wl.k_pool)
+    v2 = np.empty_like(wl.v_pool)
+    k2[perm] = wl.k_pool
+    v2[perm] = wl.v_pool
+    wl.k_pool, wl.v_pool = k2, v2
+    wl.block_tables = perm[wl.block_tables].astype(np.int32)
+    moved = run_full(P, wl).out_bits()
+    assert np.array_equal(base, moved)
+
+
+def test_run_to_run_determinism(P):
+    _, pipeline = P
+    wl = make_config("llama8b")
+    dw = pipeline.DeviceWorkload(wl)
+    dw.attention()
+    a = dw.out.clone()
+    for _ in range(3):
+        dw.out.zero_()
+        dw.attention()
+        torch.cuda.synchronize()
+        assert torch.equal(a.view(torch.int16), dw.out.view(torch.int16))
+
+
+def test_hit_rows_match_miss_rows(P):
+    # the same prompt served as a hit and as a miss
+    for prefix, suffix in ((256, 64), (37, 100), (1000, 1)):
+        invs = [Invocation(0, suffix, hit=True, suffix_key=0),
+                Invocation(0, suffix, hit=False, suffix_key=0)]
+        wl = build_workload("hitmiss", 8, [prefix], invs, num_q_heads=8, num_kv_heads=2,
+                            head_dim=128, num_blocks=256)
+        out = oracle.bf16_bits_to_f64(run_full(P, wl).out_bits())
+        hit = out[:suffix]
+        miss_tail = out[suffix + prefix:]
+        assert np.abs(hit - miss_tail).max() <= MAX_ABS
+
+
+def test_empty_batch_is_noop(P):
+    ops, _ = P
+    dev = torch.device("cuda:0")
+    z = torch.zeros((0, 8, 64), dtype=torch.bfloat16, device=dev)
+    pool = torch.zeros((4, 2, 16, 64), dtype=torch.bfloat16, device=dev)
+    bt = torch.zeros((0, 1), dtype=torch.int32, device=dev)
+    pl = torch.zeros((0,), dtype=torch.int32, device=dev)
+    cu = torch.zeros((1,), dtype=torch.int32, device=dev)
+    ops.cs_prefill_paged_attn(z, pool, pool, bt, pl, cu, z.clone(), max_q_len=0, max_kv_len=0,
+                              scale=0.125)
+    torch.cuda.synchronize()
+
+
+def test_debug_check_rejects_out_of_range_block(P, monkeypatch):
+    ops, pipeline = P
+    wl = small_batch()
+    wl.block_tables[1, 3] = wl.num_blocks + 5
+    dw = pipeline.DeviceWorkload(wl)
+    monkeypatch.setenv("CS_DEBUG_CHECK", "1")
+    with pytest.raises(ops.CacheScoutError) as ei:
+        dw.attention()
+    assert ei.value.status == ops.CS_ERR_INVALID_ARG
+    assert "block_tables[1][3]" in str(ei.value)
+
+
+def test_debug_check_accepts_valid_metadata(P, monkeypatch):
+    _, pipeline = P
+    monkeypatch.setenv("CS_DEBUG_CHECK", "1")
+    wl = small_batch()
+    dw = pipeline.DeviceWorkload(wl)
+    dw.attention()
+    torch.cuda.synchronize()
