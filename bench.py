@@ -1,0 +1,250 @@
+"""Benchmark: paged prefix-reuse prefill attention + KV prefetch on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+One step is one serving pass over the workload's agents in dispatch order:
+for each agent, its invocations run cs_prefill_paged_attn on the main stream
+while cs_kv_prefetch brings the next agent's CPU-tier anchor blocks into the
+pool on a side stream; the main stream waits on the prefetch's event before
+the next agent's attention.  Inputs are resident in HBM (and the prefetch
+sources in pinned host memory) before timing starts.
+
+Prints one JSON line.  ``value`` is the attention throughput of the whole step
+(algorithmic FLOP of all attention launches / wall time of the step);
+``roofline`` rates the attention kernel from its own average launch duration
+(HIP events on the main stream, inside the timed region); ``prefetch`` rates
+the copy from its launch durations on the side stream; ``cpu_baseline`` times
+the float64 oracle on a bounded sample of the same workload on the host.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "prefill-attn TFLOP/s (% bf16 MFMA peak) + KV prefetch GB/s, 1 MI355X"
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+PEAK_PCIE5_X16_GBS = 63.0        # PCIe 5.0 x16, one direction, 128b/130b
+KERNEL_SOURCES = ("paper_2608_14624_amd/csrc/prefill_paged_attn.hip",
+                  "paper_2608_14624_amd/csrc/kv_prefetch.hip")
+
+DESCRIPTIONS = {
+    "llama70b_prefetch": "16 invocations over 4 agents, 64 query / 8 KV heads, head_dim 128, "
+                         "cached prefix 4096 + suffix 512 tokens, 16-token blocks in a "
+                         "16384-block pool; 64 of each agent's 256 anchor blocks are "
+                         "prefetched from pinned host memory on a side stream while the "
+                         "previous agent's attention runs",
+    "llama8b": "1 request, 32 query / 8 KV heads, head_dim 128, cached prefix 2048 + suffix "
+               "1024 tokens, 16384-block pool",
+    "agent_batch": "32 invocations over 4 agents, anchors U[1536,3072], suffixes U[256,2048], "
+                   "32 query / 8 KV heads, head_dim 128, 16384-block pool",
+    "long_mixed": "128 invocations over 8 agents, anchors U[4096,8192], lognormal suffixes "
+                  "(median 512) in [128,4096], 77 hits / 51 full-prompt misses, 32 query / 8 "
+                  "KV heads, head_dim 128, pool at 90% occupancy",
+}
+
+
+def source_hash(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload, kernel_hash):
+    """HBM traffic per attention launch from a committed rocprofv3 --pmc summary.
+
+    Only used while the kernel source is the one the counters were taken on.
+    """
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    entry = data.get(workload)
+    if not entry or entry.get("kernel_sha") != kernel_hash:
+        return None
+    return entry.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, budget_s=20.0):
+    """The float64 oracle on whole invocations of the same workload, as many as
+    fit the time budget (at least one), in TFLOP/s of algorithmic work."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count()
+    kp, vp = wl.k_pool, wl.v_pool
+    if wl.prefetch_dst is not None:
+        kp, vp = oracle.kv_prefetch(wl.host_k, wl.host_v, wl.prefetch_dst, kp, vp)
+    cu = wl.cu_q_lens.astype(np.int64)
+    done_flops, elapsed, n_inv = 0, 0.0, 0
+    for r in range(wl.batch):
+        s = int(cu[r + 1] - cu[r])
+        p = int(wl.prefix_lens[r])
+        t0 = time.perf_counter()
+        oracle.prefill_paged_attn(wl.q[cu[r]:cu[r + 1]], kp, vp, wl.block_tables[r:r + 1],
+                                  wl.prefix_lens[r:r + 1], np.array([0, s]), wl.num_q_heads,
+                                  wl.num_kv_heads, wl.scale)
+        elapsed += time.perf_counter() - t0
+        done_flops += 4 * wl.head_dim * wl.num_q_heads * (s * p + s * (s + 1) // 2)
+        n_inv += 1
+        if elapsed >= budget_s:
+            break
+    return {"value": done_flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{n_inv} of {wl.batch} invocations of {wl.name}, full float64 "
+                      f"oracle ({elapsed:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama70b_prefetch",
+                    choices=sorted(DESCRIPTIONS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run only a plain 1 GiB device-to-device copy (the reference kernel "
+                         "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path "
+              "shards by KV head or by invocation with no exchange inside it, see the "
+              "design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_14624_amd import pipeline
+    from paper_2608_14624_amd.workload import make_config
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    if args.copy_probe:
+        nbytes = 1 << 30
+        src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=dev).normal_()
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": nbytes, "copy_probe_bytes_written": nbytes,
+                          "launches": 5}), flush=True)
+        return
+    wl = make_config(args.workload)
+    dw = pipeline.DeviceWorkload(wl, dev)
+    main_stream = torch.cuda.current_stream(dev)
+    if wl.prefetch_dst is not None:
+        # serving order with the next agent's prefetch overlapped on a side stream
+        pipe = pipeline.AgentPipeline(dw)
+        pipe.stage_first()
+        n_launch = len(pipe.agents)
+        step_flops, step_bytes, warm = pipe.flops, pipe.prefetch_bytes, pipe.step
+    else:
+        # no CPU-tier blocks: the whole batch is one attention launch
+        pipe = None
+        n_launch = 1
+        step_flops, step_bytes, warm = wl.flops(), 0, dw.attention
+    for _ in range(args.warmup):
+        warm()
+    torch.cuda.synchronize()
+
+    # per-launch events: attention on the main stream, prefetch on the side stream
+    def events():
+        return [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in range(n_launch)] for _ in range(args.steps)]
+    a_ev, p_ev = events(), events()
+
+    def timed_step(si):
+        if pipe is None:
+            a_ev[si][0][0].record(main_stream)
+            dw.attention(stream=main_stream)
+            a_ev[si][0][1].record(main_stream)
+            return
+        # same order as AgentPipeline.step, with events around each launch
+        for k, a in enumerate(pipe.agents):
+            nxt = pipe.agents[(k + 1) % n_launch]
+            if k == 0:
+                pipe.side.wait_stream(main_stream)
+            with torch.cuda.stream(pipe.side):
+                p_ev[si][k][0].record(pipe.side)
+                pipe.prefetch_agent(nxt, pipe.side)
+                p_ev[si][k][1].record(pipe.side)
+                pipe.events[nxt].record(pipe.side)
+            a_ev[si][k][0].record(main_stream)
+            pipe.batches[k].attention(stream=main_stream)
+            a_ev[si][k][1].record(main_stream)
+            main_stream.wait_event(pipe.events[nxt])
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for si in range(args.steps):
+        timed_step(si)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    ms_per_step = wall / args.steps * 1e3
+    value = step_flops * args.steps / wall / 1e12
+    attn_ms = sum(e0.elapsed_time(e1) for row in a_ev for e0, e1 in row)
+    n_attn = args.steps * n_launch
+    attn_avg_ms = attn_ms / n_attn
+    achieved = step_flops * args.steps / (attn_ms * 1e-3) / 1e12
+    pf_bytes_per_step = step_bytes
+    prefetch = None
+    if pf_bytes_per_step:
+        pf_ms = [e0.elapsed_time(e1) for row in p_ev for e0, e1 in row]
+        pf_gbs = pf_bytes_per_step * args.steps / (sum(pf_ms) * 1e-3) / 1e9
+        prefetch = {"value": round(pf_gbs, 2), "unit": "GB/s",
+                    "frac_link": round(pf_gbs / PEAK_PCIE5_X16_GBS, 4),
+                    "link_peak": PEAK_PCIE5_X16_GBS, "frac_hbm": round(pf_gbs / PEAK_HBM_GBS, 5),
+                    "bytes_per_step": pf_bytes_per_step, "launches_per_step": n_launch,
+                    "avg_launch_us": round(sum(pf_ms) / len(pf_ms) * 1e3, 2),
+                    "overlapped_with_attention": True}
+    khash = source_hash(KERNEL_SOURCES[:1])
+    traffic = load_traffic(args.workload, khash)
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {DESCRIPTIONS[args.workload]}",
+                   "attention_flop_per_step": step_flops,
+                   "attention_launches_per_step": n_launch,
+                   "total_q": wl.total_q, "num_blocks": wl.num_blocks},
+        "frac_of_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                     "kernel": "prefill_paged_attn_kernel<128>",
+                     "avg_launch_us": round(attn_avg_ms * 1e3, 2),
+                     "flop_per_launch": step_flops // n_launch},
+        "prefetch": prefetch,
+        "kernel_sha": khash,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
