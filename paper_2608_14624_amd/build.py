@@ -32,6 +32,9 @@ def build(verbose=False):
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
            # keep the compiler from forming packed fp32 ops
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           # MFMA accumulators in arch VGPRs: the softmax rescale then works on
+           # them in place instead of copying them out of AGPRs every step
+           "-mllvm", "-amdgpu-mfma-vgpr-form",
            "-Wall", "-Wno-unused-result",
            "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG_DIR, "csrc"),
            *sources, "-o", tmp]

@@ -129,64 +129,93 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     qreg[ks] = as_bf16x8(v);
   }
 
+  // ---- staging: wave w moves pool block (4*step + w) of the key range ----
+  // The block id is wave-uniform and read with a scalar load one step ahead,
+  // so the vector loads of a step never wait on a block-table lookup.
+  // K: lane l moves chunks c = l + 64u: token c / (D/8), dims (c % (D/8))*8..+7
+  // V: lane l < 4*(D/8) moves tokens 4*(l / (D/8)) .. +3, dims (l % (D/8))*8..+7
+  constexpr int kChunksPerRow = D / 8;
+  constexpr int kKLoads = kBlock * kChunksPerRow / 64;             // 4 (D=128), 2 (D=64)
+  constexpr int kVLanes = (kBlock / 4) * kChunksPerRow;            // 64 or 32
+  const bool v_active = lane < kVLanes;
+  const int v_quad = lane / kChunksPerRow;
+  const int v_dc = lane % kChunksPerRow;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const __attribute__((address_space(4))) int32_t* bt_c =
+      (const __attribute__((address_space(4))) int32_t*)bt;
+  auto block_id = [&](int step) -> int {
+    const int lb = step * (kBN / kBlock) + wave_u;
+    return lb < n_blk ? bt_c[lb] : -1;                               // -1: past the end
+  };
+
+  uint4 kreg[kKLoads];
+  uint4 vreg[4];
+  auto load_step = [&](int id) {
+    if (id >= 0) {
+      const uint16_t* kb = kbase + (size_t)id * slot_elems;
+      const uint16_t* vb = vbase + (size_t)id * slot_elems;
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) {
+        const int c = lane + 64 * u;
+        kreg[u] = *reinterpret_cast<const uint4*>(kb + (c / kChunksPerRow) * D + (c % kChunksPerRow) * 8);
+      }
+      if (v_active) {
+        const uint16_t* src = vb + (v_quad * 4) * D + v_dc * 8;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) vreg[u] = *reinterpret_cast<const uint4*>(src + u * D);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) kreg[u] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) vreg[u] = make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_step = [&]() {
+#pragma unroll
+    for (int u = 0; u < kKLoads; ++u) {
+      const int c = lane + 64 * u;
+      const int key = wave_u * kBlock + c / kChunksPerRow;
+      *reinterpret_cast<uint4*>(&sm.k[key * kStride + (c % kChunksPerRow) * 8]) = kreg[u];
+    }
+    if (v_active) {
+      // transpose 4 keys x 8 dims into 8 rows of V^T, 4 keys (8 bytes) each
+      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
+      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
+      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
+      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
+      const int col = wave_u * kBlock + v_quad * 4;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        // byte selectors: low halves (even dims) or high halves (odd dims)
+        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t lo = __builtin_amdgcn_perm(w1[e >> 1], w0[e >> 1], sel);
+        const uint32_t hi = __builtin_amdgcn_perm(w3[e >> 1], w2[e >> 1], sel);
+        *reinterpret_cast<uint2*>(&sm.vt[(v_dc * 8 + e) * vStride + col]) = make_uint2(lo, hi);
+      }
+    }
+  };
+
   f32x16 oacc[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
-  float m_run = -INFINITY;
-  float l_run = 0.f;
+  float m_run = -INFINITY;     // running max of the raw (unscaled) logits
+  float l_run = 0.f;           // this lane's partial row sum (its half of the keys)
+  const float c = p.scale_log2;
+  // first key position that some row of this wave cannot see
+  const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
 
+  int id_next = block_id(1);
+  load_step(block_id(0));
   for (int step = 0; step < n_steps; ++step) {
     const int kstart = step * kBN;
     __syncthreads();   // previous step's LDS reads are done
-
-    // ---- stage K [key][d] ------------------------------------------
-    constexpr int kChunksPerRow = D / 8;
-    constexpr int kChunks = kBN * kChunksPerRow;
-#pragma unroll
-    for (int c = tid; c < kChunks; c += kThreads) {
-      const int key = c / kChunksPerRow;
-      const int dc = c % kChunksPerRow;
-      const int j = kstart + key;
-      const int lb = j / kBlock;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (lb < n_blk) {
-        const size_t slot = (size_t)bt[lb];
-        v = *reinterpret_cast<const uint4*>(kbase + slot * slot_elems + (j % kBlock) * D + dc * 8);
-      }
-      *reinterpret_cast<uint4*>(&sm.k[key * kStride + dc * 8]) = v;
-    }
-    // ---- stage V^T [d][key]: each item moves 4 keys x 8 dims --------
-    constexpr int kItems = (kBN / 4) * kChunksPerRow;
-#pragma unroll
-    for (int c = tid; c < kItems; c += kThreads) {
-      const int quad = c / kChunksPerRow;
-      const int dc = c % kChunksPerRow;
-      const int j0 = kstart + quad * 4;        // 4 keys inside one block
-      const int lb = j0 / kBlock;
-      uint4 v[4] = {make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0),
-                    make_uint4(0, 0, 0, 0), make_uint4(0, 0, 0, 0)};
-      if (lb < n_blk) {
-        const size_t slot = (size_t)bt[lb];
-        const uint16_t* src = vbase + slot * slot_elems + (j0 % kBlock) * D + dc * 8;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const uint4*>(src + u * D);
-      }
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&v[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&v[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&v[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&v[3]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int sh = (e & 1) * 16;
-        const uint32_t a0 = (w0[e >> 1] >> sh) & 0xffffu;
-        const uint32_t a1 = (w1[e >> 1] >> sh) & 0xffffu;
-        const uint32_t a2 = (w2[e >> 1] >> sh) & 0xffffu;
-        const uint32_t a3 = (w3[e >> 1] >> sh) & 0xffffu;
-        uint2 packed = make_uint2(a0 | (a1 << 16), a2 | (a3 << 16));
-        *reinterpret_cast<uint2*>(&sm.vt[(dc * 8 + e) * vStride + quad * 4]) = packed;
-      }
-    }
+    store_step();
     __syncthreads();
+    if (step + 1 < n_steps) {
+      load_step(id_next);                 // in flight during the math below
+      id_next = block_id(step + 2);
+    }
 
     // ---- S^T = K Q^T: two 32-key tiles ------------------------------
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
@@ -199,33 +228,43 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
       }
     }
 
-    // ---- mask, running max ------------------------------------------
+    // ---- mask (only where some key of the step is past a row's limit) --
     // accumulator register rr of tile mt holds key
     //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
+    if (kstart + kBN - 1 > wave_qmin) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
+          sacc[mt][rr] = (kj <= qpos) ? sacc[mt][rr] : -INFINITY;
+        }
+      }
+    }
     float mloc = -INFINITY;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
-        float s = sacc[mt][rr] * p.scale_log2;
-        s = (kj <= qpos) ? s : -INFINITY;
-        sacc[mt][rr] = s;
-        mloc = fmaxf(mloc, s);
-      }
+      for (int rr = 0; rr < 16; ++rr) mloc = fmaxf(mloc, sacc[mt][rr]);
     }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-    const float m_new = fmaxf(m_run, mloc);     // finite: key 0 is visible to every row
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
+    // ---- lazy rescale: move the reference max only when a row's max grew
+    // by more than 2^8 in probability; otherwise keep it (p <= 256 then)
+    const bool grow = (mloc - m_run) * c > 8.f;      // true for every row at step 0
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+      const float m_new = grow ? mloc : m_run;
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      m_run = m_new;
+      l_run *= alpha;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+    }
+    const float mc = m_run * c;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
-        const float e = __builtin_amdgcn_exp2f(sacc[mt][rr] - m_new);
+        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][rr], c, -mc));
         sacc[mt][rr] = e;
         l_run += e;
       }
