@@ -72,8 +72,8 @@ template <int D>
 struct Lds {
   static constexpr int kStride = D + 8;       // K rows: [key][d], 16 B pad
   static constexpr int vStride = kBN + 4;     // V^T rows: [d][key], 8 B pad
-  uint16_t k[kBN * kStride];
-  uint16_t vt[D * vStride];
+  uint16_t k[2][kBN * kStride];               // K of steps j (even/odd buffer)
+  uint16_t vt[2][D * vStride];                // V^T of steps j
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -133,13 +133,16 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   // The block id is wave-uniform and read with a scalar load one step ahead,
   // so the vector loads of a step never wait on a block-table lookup.
   // K: lane l moves chunks c = l + 64u: token c / (D/8), dims (c % (D/8))*8..+7
-  // V: lane l < 4*(D/8) moves tokens 4*(l / (D/8)) .. +3, dims (l % (D/8))*8..+7
+  // V: lane l < 4*(D/8) moves tokens 4*(l % 4) .. +3, dims (l / 4)*8..+7.
+  //    Taking the token quad from the low lane bits spreads each 16-lane
+  //    group of the transposed 8-byte LDS writes over 8 bank pairs (rows
+  //    8 apart alone would land on 2 bank pairs of the padded V^T rows).
   constexpr int kChunksPerRow = D / 8;
   constexpr int kKLoads = kBlock * kChunksPerRow / 64;             // 4 (D=128), 2 (D=64)
   constexpr int kVLanes = (kBlock / 4) * kChunksPerRow;            // 64 or 32
   const bool v_active = lane < kVLanes;
-  const int v_quad = lane / kChunksPerRow;
-  const int v_dc = lane % kChunksPerRow;
+  const int v_quad = lane & 3;
+  const int v_dc = lane >> 2;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const __attribute__((address_space(4))) int32_t* bt_c =
       (const __attribute__((address_space(4))) int32_t*)bt;
@@ -148,36 +151,46 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     return lb < n_blk ? bt_c[lb] : -1;                               // -1: past the end
   };
 
+  // K runs one step ahead of V: iteration j reads K_{j+1} (for the next
+  // step's logits) and V_j (for this step's PV product) and writes K_{j+2}
+  // and V_{j+1} into the other halves of the two double buffers, so one
+  // barrier per step separates every write from the reads it must follow.
   uint4 kreg[kKLoads];
   uint4 vreg[4];
-  auto load_step = [&](int id) {
+  auto load_k = [&](int id) {
     if (id >= 0) {
       const uint16_t* kb = kbase + (size_t)id * slot_elems;
-      const uint16_t* vb = vbase + (size_t)id * slot_elems;
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
         const int c = lane + 64 * u;
         kreg[u] = *reinterpret_cast<const uint4*>(kb + (c / kChunksPerRow) * D + (c % kChunksPerRow) * 8);
       }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) kreg[u] = make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto load_v = [&](int id) {
+    if (id >= 0) {
       if (v_active) {
-        const uint16_t* src = vb + (v_quad * 4) * D + v_dc * 8;
+        const uint16_t* src = vbase + (size_t)id * slot_elems + (v_quad * 4) * D + v_dc * 8;
 #pragma unroll
         for (int u = 0; u < 4; ++u) vreg[u] = *reinterpret_cast<const uint4*>(src + u * D);
       }
     } else {
 #pragma unroll
-      for (int u = 0; u < kKLoads; ++u) kreg[u] = make_uint4(0, 0, 0, 0);
-#pragma unroll
       for (int u = 0; u < 4; ++u) vreg[u] = make_uint4(0, 0, 0, 0);
     }
   };
-  auto store_step = [&]() {
+  auto store_k = [&](uint16_t* kbuf) {
 #pragma unroll
     for (int u = 0; u < kKLoads; ++u) {
       const int c = lane + 64 * u;
       const int key = wave_u * kBlock + c / kChunksPerRow;
-      *reinterpret_cast<uint4*>(&sm.k[key * kStride + (c % kChunksPerRow) * 8]) = kreg[u];
+      *reinterpret_cast<uint4*>(&kbuf[key * kStride + (c % kChunksPerRow) * 8]) = kreg[u];
     }
+  };
+  auto store_v = [&](uint16_t* vbuf) {
     if (v_active) {
       // transpose 4 keys x 8 dims into 8 rows of V^T, 4 keys (8 bytes) each
       const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
@@ -191,7 +204,20 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
         const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
         const uint32_t lo = __builtin_amdgcn_perm(w1[e >> 1], w0[e >> 1], sel);
         const uint32_t hi = __builtin_amdgcn_perm(w3[e >> 1], w2[e >> 1], sel);
-        *reinterpret_cast<uint2*>(&sm.vt[(v_dc * 8 + e) * vStride + col]) = make_uint2(lo, hi);
+        *reinterpret_cast<uint2*>(&vbuf[(v_dc * 8 + e) * vStride + col]) = make_uint2(lo, hi);
+      }
+    }
+  };
+  // S^T = K Q^T for the 64 keys in kbuf: two 32-key tiles
+  auto logits = [&](const uint16_t* kbuf, f32x16* sacc) {
+    sacc[0] = f32x16{};
+    sacc[1] = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const uint4 a = *reinterpret_cast<const uint4*>(&kbuf[(mt * 32 + qi) * kStride + ks * 16 + half * 8]);
+        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], sacc[mt], 0, 0, 0);
       }
     }
   };
@@ -205,28 +231,37 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   // first key position that some row of this wave cannot see
   const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
 
-  int id_next = block_id(1);
-  load_step(block_id(0));
-  for (int step = 0; step < n_steps; ++step) {
-    const int kstart = step * kBN;
-    __syncthreads();   // previous step's LDS reads are done
-    store_step();
-    __syncthreads();
-    if (step + 1 < n_steps) {
-      load_step(id_next);                 // in flight during the math below
-      id_next = block_id(step + 2);
-    }
+  // ---- prologue: K_0, V_0, K_1 in LDS; K_2, V_1 in registers ---------
+  load_k(block_id(0));
+  load_v(block_id(0));
+  store_k(sm.k[0]);
+  store_v(sm.vt[0]);
+  if (n_steps > 1) {
+    load_k(block_id(1));
+    store_k(sm.k[1]);
+  }
+  if (n_steps > 2) load_k(block_id(2));
+  if (n_steps > 1) load_v(block_id(1));
+  int id_k = block_id(3);      // K of step j+3, read at iteration j
+  int id_v = block_id(2);      // V of step j+2
+  __syncthreads();
+  f32x16 s_cur[2];
+  logits(sm.k[0], s_cur);
 
-    // ---- S^T = K Q^T: two 32-key tiles ------------------------------
-    f32x16 sacc[2] = {f32x16{}, f32x16{}};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-        const uint4 a = *reinterpret_cast<const uint4*>(&sm.k[(mt * 32 + qi) * kStride + ks * 16 + half * 8]);
-        sacc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], sacc[mt], 0, 0, 0);
-      }
-    }
+  for (int j = 0; j < n_steps; ++j) {
+    const int kstart = j * kBN;
+    const int cur = j & 1;
+    __syncthreads();   // iteration j-1's reads are done and its writes visible
+    if (j + 2 < n_steps) store_k(sm.k[cur]);         // K_{j+2}
+    if (j + 1 < n_steps) store_v(sm.vt[cur ^ 1]);    // V_{j+1}
+    if (j + 3 < n_steps) load_k(id_k);               // in flight for one step
+    if (j + 2 < n_steps) load_v(id_v);
+    id_k = block_id(j + 4);
+    id_v = block_id(j + 3);
+
+    // logits of the next step (MFMA) overlap this step's softmax (VALU)
+    f32x16 s_next[2];
+    if (j + 1 < n_steps) logits(sm.k[cur ^ 1], s_next);
 
     // ---- mask (only where some key of the step is past a row's limit) --
     // accumulator register rr of tile mt holds key
@@ -237,7 +272,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
           const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
-          sacc[mt][rr] = (kj <= qpos) ? sacc[mt][rr] : -INFINITY;
+          s_cur[mt][rr] = (kj <= qpos) ? s_cur[mt][rr] : -INFINITY;
         }
       }
     }
@@ -245,7 +280,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) mloc = fmaxf(mloc, sacc[mt][rr]);
+      for (int rr = 0; rr < 16; ++rr) mloc = fmaxf(mloc, s_cur[mt][rr]);
     }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     // ---- lazy rescale: move the reference max only when a row's max grew
@@ -264,29 +299,32 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) {
-        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[mt][rr], c, -mc));
-        sacc[mt][rr] = e;
+        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mt][rr], c, -mc));
+        s_cur[mt][rr] = e;
         l_run += e;
       }
     }
 
     // ---- O^T += V^T P^T: four 16-key MFMA steps --------------------
+    const uint16_t* vbuf = sm.vt[cur];
 #pragma unroll
     for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
       const int mt = ks2 >> 1;
       const int rb = (ks2 & 1) * 8;
       bf16x8 b;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) b[s] = (__bf16)sacc[mt][rb + s];
+      for (int s2 = 0; s2 < 8; ++s2) b[s2] = (__bf16)s_cur[mt][rb + s2];
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t* vrow = &sm.vt[(dt * 32 + qi) * vStride + ks2 * 16 + 4 * half];
+        const uint16_t* vrow = &vbuf[(dt * 32 + qi) * vStride + ks2 * 16 + 4 * half];
         const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
         const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
         const uint4 a = make_uint4(lo.x, lo.y, hi.x, hi.y);
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), b, oacc[dt], 0, 0, 0);
       }
     }
+    s_cur[0] = s_next[0];
+    s_cur[1] = s_next[1];
   }
 
   // ---- epilogue: O / l, bf16, store --------------------------------
