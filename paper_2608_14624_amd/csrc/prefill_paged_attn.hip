@@ -39,6 +39,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kBlock = 16;    // tokens per pool block
@@ -77,6 +78,30 @@ struct Lds {
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Lanes l and l ^ 32 hold the same query row (the two halves of its keys).
+// v_permlane32_swap exchanges the upper lane half of its first operand with
+// the lower lane half of its second, in VALU without an LDS round trip; with
+// both operands holding x, the first then holds (x_lo, x_lo) and the second
+// (x_hi, x_hi), so every lane sees its own value and its partner's.  The
+// clang builtin of this ROCm returns the first operand for both results, so
+// the instruction is written out; the s_nops cover the VALU-write /
+// permlane-read hazard the compiler cannot see inside inline asm.
+__device__ __forceinline__ void pair_swap(float x, float& a, float& b) {
+  a = x;
+  b = x;
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ float pair_max(float x) {
+  float a, b;
+  pair_swap(x, a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  float a, b;
+  pair_swap(x, a, b);
+  return a + b;
+}
 
 template <int D>
 __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) {
@@ -226,7 +251,6 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
   float m_run = -INFINITY;     // running max of the raw (unscaled) logits
-  float l_run = 0.f;           // this lane's partial row sum (its half of the keys)
   const float c = p.scale_log2;
   // first key position that some row of this wave cannot see
   const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
@@ -245,10 +269,12 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   int id_k = block_id(3);      // K of step j+3, read at iteration j
   int id_v = block_id(2);      // V of step j+2
   __syncthreads();
-  f32x16 s_cur[2];
-  logits(sm.k[0], s_cur);
+  f32x16 s_a[2], s_b[2];
+  logits(sm.k[0], s_a);
+  float l_part[4] = {0.f, 0.f, 0.f, 0.f};     // partial row sums (short add chains)
 
-  for (int j = 0; j < n_steps; ++j) {
+  // One step: consume logits s_cur of step j, produce logits s_next of step j+1.
+  auto step = [&](const int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2]) {
     const int kstart = j * kBN;
     const int cur = j & 1;
     __syncthreads();   // iteration j-1's reads are done and its writes visible
@@ -259,9 +285,10 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     id_k = block_id(j + 4);
     id_v = block_id(j + 3);
 
-    // logits of the next step (MFMA) overlap this step's softmax (VALU)
-    f32x16 s_next[2];
-    if (j + 1 < n_steps) logits(sm.k[cur ^ 1], s_next);
+    // The logits of the next step are issued first: the MFMA pipe works on
+    // them while this step's max, exponentials and row sums run on the VALU.
+    // On the last step they read a stale K buffer and are discarded.
+    logits(sm.k[cur ^ 1], s_next);
 
     // ---- mask (only where some key of the step is past a row's limit) --
     // accumulator register rr of tile mt holds key
@@ -282,7 +309,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) mloc = fmaxf(mloc, s_cur[mt][rr]);
     }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    mloc = pair_max(mloc);
     // ---- lazy rescale: move the reference max only when a row's max grew
     // by more than 2^8 in probability; otherwise keep it (p <= 256 then)
     const bool grow = (mloc - m_run) * c > 8.f;      // true for every row at step 0
@@ -290,19 +317,18 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
       const float m_new = grow ? mloc : m_run;
       const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
       m_run = m_new;
-      l_run *= alpha;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
     }
+
     const float mc = m_run * c;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-      for (int rr = 0; rr < 16; ++rr) {
-        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mt][rr], c, -mc));
-        s_cur[mt][rr] = e;
-        l_run += e;
-      }
+      for (int rr = 0; rr < 16; ++rr)
+        s_cur[mt][rr] = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mt][rr], c, -mc));
     }
 
     // ---- O^T += V^T P^T: four 16-key MFMA steps --------------------
@@ -314,6 +340,13 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
       bf16x8 b;
 #pragma unroll
       for (int s2 = 0; s2 < 8; ++s2) b[s2] = (__bf16)s_cur[mt][rb + s2];
+      // row sum over the same bf16 probabilities the PV product uses,
+      // two per instruction
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+      l_part[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 0, 1), ones, l_part[0], false);
+      l_part[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 2, 3), ones, l_part[1], false);
+      l_part[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 4, 5), ones, l_part[2], false);
+      l_part[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 6, 7), ones, l_part[3], false);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const uint16_t* vrow = &vbuf[(dt * 32 + qi) * vStride + ks2 * 16 + 4 * half];
@@ -323,12 +356,17 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), b, oacc[dt], 0, 0, 0);
       }
     }
-    s_cur[0] = s_next[0];
-    s_cur[1] = s_next[1];
+  };
+
+  // unrolled by two so the logits ping-pong between s_a and s_b without copies
+  for (int j = 0; j < n_steps; j += 2) {
+    step(j, s_a, s_b);
+    if (j + 1 < n_steps) step(j + 1, s_b, s_a);
   }
+  const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
 
   // ---- epilogue: O / l, bf16, store --------------------------------
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = pair_sum(l_run);
   const float inv = 1.f / l_tot;
   if (row_valid) {
     uint16_t* orow = p.out + qrow;
