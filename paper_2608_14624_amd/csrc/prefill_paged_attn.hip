@@ -40,7 +40,9 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kBlock = 16;    // tokens per pool block
 constexpr int kBN = 64;       // keys per step
@@ -72,9 +74,11 @@ struct Params {
 template <int D>
 struct Lds {
   static constexpr int kStride = D + 8;       // K rows: [key][d], 16 B pad
-  static constexpr int vStride = kBN + 4;     // V^T rows: [d][key], 8 B pad
+  // V rows [key][d] padded by 32 B: the transposing reads of a 16-lane group
+  // (4 keys x 4 column quads) land on distinct banks.
+  static constexpr int vStride = D + 16;
   uint16_t k[2][kBN * kStride];               // K of steps j (even/odd buffer)
-  uint16_t vt[2][D * vStride];                // V^T of steps j
+  uint16_t v[2][kBN * vStride];               // V of steps j
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
@@ -156,18 +160,11 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
 
   // ---- staging: wave w moves pool block (4*step + w) of the key range ----
   // The block id is wave-uniform and read with a scalar load one step ahead,
-  // so the vector loads of a step never wait on a block-table lookup.
-  // K: lane l moves chunks c = l + 64u: token c / (D/8), dims (c % (D/8))*8..+7
-  // V: lane l < 4*(D/8) moves tokens 4*(l % 4) .. +3, dims (l / 4)*8..+7.
-  //    Taking the token quad from the low lane bits spreads each 16-lane
-  //    group of the transposed 8-byte LDS writes over 8 bank pairs (rows
-  //    8 apart alone would land on 2 bank pairs of the padded V^T rows).
+  // so the vector loads of a step never wait on a block-table lookup.  K and
+  // V tiles are both moved row-major: lane l moves chunks c = l + 64u, token
+  // c / (D/8), dims (c % (D/8))*8 .. +7.
   constexpr int kChunksPerRow = D / 8;
   constexpr int kKLoads = kBlock * kChunksPerRow / 64;             // 4 (D=128), 2 (D=64)
-  constexpr int kVLanes = (kBlock / 4) * kChunksPerRow;            // 64 or 32
-  const bool v_active = lane < kVLanes;
-  const int v_quad = lane & 3;
-  const int v_dc = lane >> 2;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const __attribute__((address_space(4))) int32_t* bt_c =
       (const __attribute__((address_space(4))) int32_t*)bt;
@@ -181,7 +178,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   // and V_{j+1} into the other halves of the two double buffers, so one
   // barrier per step separates every write from the reads it must follow.
   uint4 kreg[kKLoads];
-  uint4 vreg[4];
+  uint4 vreg[kKLoads];
   auto load_k = [&](int id) {
     if (id >= 0) {
       const uint16_t* kb = kbase + (size_t)id * slot_elems;
@@ -197,14 +194,15 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   };
   auto load_v = [&](int id) {
     if (id >= 0) {
-      if (v_active) {
-        const uint16_t* src = vbase + (size_t)id * slot_elems + (v_quad * 4) * D + v_dc * 8;
+      const uint16_t* vb = vbase + (size_t)id * slot_elems;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) vreg[u] = *reinterpret_cast<const uint4*>(src + u * D);
+      for (int u = 0; u < kKLoads; ++u) {
+        const int c = lane + 64 * u;
+        vreg[u] = *reinterpret_cast<const uint4*>(vb + (c / kChunksPerRow) * D + (c % kChunksPerRow) * 8);
       }
     } else {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) vreg[u] = make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < kKLoads; ++u) vreg[u] = make_uint4(0, 0, 0, 0);
     }
   };
   auto store_k = [&](uint16_t* kbuf) {
@@ -216,22 +214,28 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     }
   };
   auto store_v = [&](uint16_t* vbuf) {
-    if (v_active) {
-      // transpose 4 keys x 8 dims into 8 rows of V^T, 4 keys (8 bytes) each
-      const uint32_t* w0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
-      const uint32_t* w1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
-      const uint32_t* w2 = reinterpret_cast<const uint32_t*>(&vreg[2]);
-      const uint32_t* w3 = reinterpret_cast<const uint32_t*>(&vreg[3]);
-      const int col = wave_u * kBlock + v_quad * 4;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        // byte selectors: low halves (even dims) or high halves (odd dims)
-        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-        const uint32_t lo = __builtin_amdgcn_perm(w1[e >> 1], w0[e >> 1], sel);
-        const uint32_t hi = __builtin_amdgcn_perm(w3[e >> 1], w2[e >> 1], sel);
-        *reinterpret_cast<uint2*>(&vbuf[(v_dc * 8 + e) * vStride + col]) = make_uint2(lo, hi);
-      }
+    for (int u = 0; u < kKLoads; ++u) {
+      const int c = lane + 64 * u;
+      const int key = wave_u * kBlock + c / kChunksPerRow;
+      *reinterpret_cast<uint4*>(&vbuf[key * vStride + (c % kChunksPerRow) * 8]) = vreg[u];
     }
+  };
+  // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
+  // transposing reads.  ds_read_b64_tr_b16 treats the 8-byte rows addressed
+  // by the 16 lanes of a group as a 16 x 4 matrix M and hands lane j of the
+  // group M[4e + j/4][j%4], e = 0..3.  Lane 16g + i addresses key
+  // 4*(g/2) + i/4 and dims 16*(g%2) + 4*(i%4) .. +3, so lane l receives
+  // V[4*(l/32) + e][32*dt + l%32], e = 0..3: the A-operand slots 0..3 (keys
+  // 4*half + e); the second read, 8 keys further, fills slots 4..7.
+  const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  auto v_frag = [&](const uint16_t* vbuf, int ks2, int dt) -> bf16x8 {
+    const uint16_t* base = &vbuf[(16 * ks2 + tr_row) * vStride + 32 * dt + tr_col];
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 8 * vStride));
+    const i16x4 lohi[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8, lohi);
   };
   // S^T = K Q^T for the 64 keys in kbuf: two 32-key tiles
   auto logits = [&](const uint16_t* kbuf, f32x16* sacc) {
@@ -259,7 +263,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   load_k(block_id(0));
   load_v(block_id(0));
   store_k(sm.k[0]);
-  store_v(sm.vt[0]);
+  store_v(sm.v[0]);
   if (n_steps > 1) {
     load_k(block_id(1));
     store_k(sm.k[1]);
@@ -279,7 +283,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     const int cur = j & 1;
     __syncthreads();   // iteration j-1's reads are done and its writes visible
     if (j + 2 < n_steps) store_k(sm.k[cur]);         // K_{j+2}
-    if (j + 1 < n_steps) store_v(sm.vt[cur ^ 1]);    // V_{j+1}
+    if (j + 1 < n_steps) store_v(sm.v[cur ^ 1]);     // V_{j+1}
     if (j + 3 < n_steps) load_k(id_k);               // in flight for one step
     if (j + 2 < n_steps) load_v(id_v);
     id_k = block_id(j + 4);
@@ -332,7 +336,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     }
 
     // ---- O^T += V^T P^T: four 16-key MFMA steps --------------------
-    const uint16_t* vbuf = sm.vt[cur];
+    const uint16_t* vbuf = sm.v[cur];
 #pragma unroll
     for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
       const int mt = ks2 >> 1;
@@ -348,13 +352,8 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
       l_part[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 4, 5), ones, l_part[2], false);
       l_part[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 6, 7), ones, l_part[3], false);
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t* vrow = &vbuf[(dt * 32 + qi) * vStride + ks2 * 16 + 4 * half];
-        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
-        const uint4 a = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), b, oacc[dt], 0, 0, 0);
-      }
+      for (int dt = 0; dt < DT; ++dt)
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), b, oacc[dt], 0, 0, 0);
     }
   };
 
