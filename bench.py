@@ -204,13 +204,28 @@ def main():
     prefetch = None
     if pf_bytes_per_step:
         pf_ms = [e0.elapsed_time(e1) for row in p_ev for e0, e1 in row]
+        # the same copies with nothing else on the GPU (after the timed region)
+        iso_ms = []
+        for _ in range(3):
+            for a in pipe.agents:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(main_stream)
+                pipe.prefetch_agent(a, main_stream)
+                e1.record(main_stream)
+                iso_ms.append((e0, e1))
+        torch.cuda.synchronize()
+        iso = sum(e0.elapsed_time(e1) for e0, e1 in iso_ms) / len(iso_ms)
+        iso_gbs = pf_bytes_per_step / n_launch / (iso * 1e-3) / 1e9
         pf_gbs = pf_bytes_per_step * args.steps / (sum(pf_ms) * 1e-3) / 1e9
         prefetch = {"value": round(pf_gbs, 2), "unit": "GB/s",
                     "frac_link": round(pf_gbs / PEAK_PCIE5_X16_GBS, 4),
                     "link_peak": PEAK_PCIE5_X16_GBS, "frac_hbm": round(pf_gbs / PEAK_HBM_GBS, 5),
                     "bytes_per_step": pf_bytes_per_step, "launches_per_step": n_launch,
                     "avg_launch_us": round(sum(pf_ms) / len(pf_ms) * 1e3, 2),
-                    "overlapped_with_attention": True}
+                    "overlapped_with_attention": True,
+                    "isolated": {"value": round(iso_gbs, 2), "unit": "GB/s",
+                                 "frac_link": round(iso_gbs / PEAK_PCIE5_X16_GBS, 4),
+                                 "avg_launch_us": round(iso * 1e3, 2)}}
     khash = source_hash(KERNEL_SOURCES[:1])
     traffic = load_traffic(args.workload, khash)
     result = {
