@@ -74,9 +74,10 @@ struct Params {
 template <int D>
 struct Lds {
   static constexpr int kStride = D + 8;       // K rows: [key][d], 16 B pad
-  // V rows [key][d] padded by 32 B: the transposing reads of a 16-lane group
-  // (4 keys x 4 column quads) land on distinct banks.
-  static constexpr int vStride = D + 16;
+  // V rows [key][d] padded by 64 B: a transposing read serves 32 lanes per
+  // cycle from 64 banks, and those lanes cover 4 keys x 64 bytes; with rows
+  // 64 bytes apart modulo 256 they hit every bank once.
+  static constexpr int vStride = D + 32;
   uint16_t k[2][kBN * kStride];               // K of steps j (even/odd buffer)
   uint16_t v[2][kBN * vStride];               // V of steps j
 };
