@@ -27,9 +27,9 @@
 //     they hold; whole blocks past the end are zero-filled in LDS, never read.
 //   * Softmax runs in base 2 with log2(e) folded into the scale.
 //
-// Work-group order: the head-tile index varies fastest, so with 8 head tiles
-// the 8 XCDs each serve one KV head and its K/V stays in that XCD's L2; token
-// tiles are issued from the last (most keys) to the first.
+// Work-group order: the KV head varies fastest, so with 8 KV heads the 8 XCDs
+// each serve one KV head and its K/V stays in that XCD's L2; token tiles are
+// issued from the last (most keys) to the first.
 #include "internal.h"
 
 #include <math.h>
@@ -123,9 +123,16 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   const int half = lane >> 5;
 
   // ---- work tile -----------------------------------------------------
+  // Work-groups are dealt to the 8 XCDs round-robin, so the KV head is the
+  // fastest-varying index: with 8 KV heads every XCD serves exactly one and
+  // keeps its K/V in its own L2.  The head tiles of that KV head come next,
+  // then invocations, then token tiles from the last (most keys) to the first.
   const int wg = blockIdx.x;
-  const int head_tile = wg % p.head_tiles;
-  const int rest = wg / p.head_tiles;
+  const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
+  const int g = wg % p.num_kv_heads;
+  const int sub = wg / p.num_kv_heads;
+  const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
+  const int rest = sub / tiles_per_kv;
   const int r = rest % p.batch;
   const int token_tile = p.token_tiles - 1 - rest / p.batch;
   const int q0 = p.cu_q_lens[r];
@@ -136,7 +143,6 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   const int L = P + S;
 
   const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
-  const int g = h / p.group;
   const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
   const bool row_valid = t < S;
   const int qpos = row_valid ? P + t : L - 1;              // last visible key
