@@ -184,48 +184,31 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   // step's logits) and V_j (for this step's PV product) and writes K_{j+2}
   // and V_{j+1} into the other halves of the two double buffers, so one
   // barrier per step separates every write from the reads it must follow.
-  uint4 kreg[kKLoads];
-  uint4 vreg[kKLoads];
-  auto load_k = [&](int id) {
+  // Two register stages: the loads of step j+3 are issued at iteration j
+  // into the stage whose data (step j+1) was just stored, so every global
+  // load has two steps to arrive.
+  using Stage = uint4[kKLoads];
+  uint4 kreg[2][kKLoads];
+  uint4 vreg[2][kKLoads];
+  auto load_tile = [&](Stage& dst, const uint16_t* base, int id) {
     if (id >= 0) {
-      const uint16_t* kb = kbase + (size_t)id * slot_elems;
+      const uint16_t* src = base + (size_t)id * slot_elems;
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
         const int c = lane + 64 * u;
-        kreg[u] = *reinterpret_cast<const uint4*>(kb + (c / kChunksPerRow) * D + (c % kChunksPerRow) * 8);
+        dst[u] = *reinterpret_cast<const uint4*>(src + (c / kChunksPerRow) * D + (c % kChunksPerRow) * 8);
       }
     } else {
 #pragma unroll
-      for (int u = 0; u < kKLoads; ++u) kreg[u] = make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < kKLoads; ++u) dst[u] = make_uint4(0, 0, 0, 0);
     }
   };
-  auto load_v = [&](int id) {
-    if (id >= 0) {
-      const uint16_t* vb = vbase + (size_t)id * slot_elems;
-#pragma unroll
-      for (int u = 0; u < kKLoads; ++u) {
-        const int c = lane + 64 * u;
-        vreg[u] = *reinterpret_cast<const uint4*>(vb + (c / kChunksPerRow) * D + (c % kChunksPerRow) * 8);
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < kKLoads; ++u) vreg[u] = make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store_k = [&](uint16_t* kbuf) {
+  auto store_tile = [&](const Stage& src, uint16_t* buf, int stride) {
 #pragma unroll
     for (int u = 0; u < kKLoads; ++u) {
       const int c = lane + 64 * u;
       const int key = wave_u * kBlock + c / kChunksPerRow;
-      *reinterpret_cast<uint4*>(&kbuf[key * kStride + (c % kChunksPerRow) * 8]) = kreg[u];
-    }
-  };
-  auto store_v = [&](uint16_t* vbuf) {
-#pragma unroll
-    for (int u = 0; u < kKLoads; ++u) {
-      const int c = lane + 64 * u;
-      const int key = wave_u * kBlock + c / kChunksPerRow;
-      *reinterpret_cast<uint4*>(&vbuf[key * vStride + (c % kChunksPerRow) * 8]) = vreg[u];
+      *reinterpret_cast<uint4*>(&buf[key * stride + (c % kChunksPerRow) * 8]) = src[u];
     }
   };
   // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
@@ -244,6 +227,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     const i16x4 lohi[2] = {lo, hi};
     return __builtin_bit_cast(bf16x8, lohi);
   };
+
   // S^T = K Q^T for the 64 keys in kbuf: two 32-key tiles
   auto logits = [&](const uint16_t* kbuf, f32x16* sacc) {
     sacc[0] = f32x16{};
@@ -266,40 +250,45 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   // first key position that some row of this wave cannot see
   const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
 
-  // ---- prologue: K_0, V_0, K_1 in LDS; K_2, V_1 in registers ---------
-  load_k(block_id(0));
-  load_v(block_id(0));
-  store_k(sm.k[0]);
-  store_v(sm.v[0]);
-  if (n_steps > 1) {
-    load_k(block_id(1));
-    store_k(sm.k[1]);
-  }
-  if (n_steps > 2) load_k(block_id(2));
-  if (n_steps > 1) load_v(block_id(1));
-  int id_k = block_id(3);      // K of step j+3, read at iteration j
-  int id_v = block_id(2);      // V of step j+2
-  __syncthreads();
-  f32x16 s_a[2], s_b[2];
-  logits(sm.k[0], s_a);
+  // ---- prologue: step 0 in LDS buffer 0; steps 1 and 2 in registers ----
   float l_part[4] = {0.f, 0.f, 0.f, 0.f};     // partial row sums (short add chains)
+  {
+    const int id0 = block_id(0);
+    load_tile(kreg[0], kbase, id0);
+    load_tile(vreg[0], vbase, id0);
+    store_tile(kreg[0], sm.k[0], kStride);
+    store_tile(vreg[0], sm.v[0], vStride);
+    if (n_steps > 1) {
+      const int id1 = block_id(1);
+      load_tile(kreg[1], kbase, id1);
+      load_tile(vreg[1], vbase, id1);
+    }
+    if (n_steps > 2) {
+      const int id2 = block_id(2);
+      load_tile(kreg[0], kbase, id2);
+      load_tile(vreg[0], vbase, id2);
+    }
+  }
+  int id_next = block_id(3);   // block id of step j+3, read at iteration j
 
-  // One step: consume logits s_cur of step j, produce logits s_next of step j+1.
-  auto step = [&](const int j, f32x16 (&s_cur)[2], f32x16 (&s_next)[2]) {
+  // One step: stage j+1 into LDS, issue the loads of step j+3, then the
+  // logits, softmax and PV product of step j.
+  auto step = [&](const int j, Stage& kst, Stage& vst) {
     const int kstart = j * kBN;
     const int cur = j & 1;
     __syncthreads();   // iteration j-1's reads are done and its writes visible
-    if (j + 2 < n_steps) store_k(sm.k[cur]);         // K_{j+2}
-    if (j + 1 < n_steps) store_v(sm.v[cur ^ 1]);     // V_{j+1}
-    if (j + 3 < n_steps) load_k(id_k);               // in flight for one step
-    if (j + 2 < n_steps) load_v(id_v);
-    id_k = block_id(j + 4);
-    id_v = block_id(j + 3);
+    if (j + 1 < n_steps) {
+      store_tile(kst, sm.k[cur ^ 1], kStride);     // K_{j+1}, V_{j+1}
+      store_tile(vst, sm.v[cur ^ 1], vStride);
+    }
+    if (j + 3 < n_steps) {                          // in flight for two steps
+      load_tile(kst, kbase, id_next);
+      load_tile(vst, vbase, id_next);
+    }
+    id_next = block_id(j + 4);
 
-    // The logits of the next step are issued first: the MFMA pipe works on
-    // them while this step's max, exponentials and row sums run on the VALU.
-    // On the last step they read a stale K buffer and are discarded.
-    logits(sm.k[cur ^ 1], s_next);
+    f32x16 s_cur[2];
+    logits(sm.k[cur], s_cur);
 
     // ---- mask (only where some key of the step is past a row's limit) --
     // accumulator register rr of tile mt holds key
@@ -364,10 +353,10 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     }
   };
 
-  // unrolled by two so the logits ping-pong between s_a and s_b without copies
+  // unrolled by two so the register stage of each step is a constant
   for (int j = 0; j < n_steps; j += 2) {
-    step(j, s_a, s_b);
-    if (j + 1 < n_steps) step(j + 1, s_b, s_a);
+    step(j, kreg[1], vreg[1]);
+    if (j + 1 < n_steps) step(j + 1, kreg[0], vreg[0]);
   }
   const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
 
