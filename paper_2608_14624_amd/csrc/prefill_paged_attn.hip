@@ -287,8 +287,14 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     }
     id_next = block_id(j + 4);
 
+    // The two waves of a SIMD (one per work-group) alternate between MFMA
+    // bursts and softmax VALU work.  A wave raises its priority while it
+    // issues MFMAs, so the matrix core is fed first and the other wave's
+    // VALU work fills the gaps instead of delaying it.
     f32x16 s_cur[2];
+    __builtin_amdgcn_s_setprio(1);
     logits(sm.k[cur], s_cur);
+    __builtin_amdgcn_s_setprio(0);
 
     // ---- mask (only where some key of the step is past a row's limit) --
     // accumulator register rr of tile mt holds key
@@ -333,6 +339,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
 
     // ---- O^T += V^T P^T: four 16-key MFMA steps --------------------
     const uint16_t* vbuf = sm.v[cur];
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
       const int mt = ks2 >> 1;
@@ -351,6 +358,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
       for (int dt = 0; dt < DT; ++dt)
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), b, oacc[dt], 0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
   };
 
   // unrolled by two so the register stage of each step is a constant
