@@ -107,6 +107,75 @@ def cpu_baseline(wl, budget_s=20.0):
                       f"oracle ({elapsed:.1f} s)"}
 
 
+def _time_launches(fn, steps, warmup, stream):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    t0 = time.perf_counter()
+    for e0, e1 in evs:
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall, sum(e0.elapsed_time(e1) for e0, e1 in evs) / steps
+
+
+def bench_copy(args, dev):
+    """The write-back scatter (HBM bound) or the offload (host-link bound) alone."""
+    import numpy as np
+    import torch
+    from paper_2608_14624_amd import ops
+    from paper_2608_14624_amd.workload import make_config
+    wl = make_config(args.workload)
+    stream = torch.cuda.current_stream(dev)
+    k_pool = torch.from_numpy(wl.k_pool.view(np.int16)).view(torch.bfloat16).to(dev)
+    v_pool = torch.from_numpy(wl.v_pool.view(np.int16)).view(torch.bfloat16).to(dev)
+    hkv, d = wl.num_kv_heads, wl.head_dim
+    if args.component == "kv_write":
+        # the suffix tokens of every invocation, written to their own slots
+        slots = []
+        for r in range(wl.batch):
+            p, s = int(wl.prefix_lens[r]), int(wl.q_lens[r])
+            j = np.arange(p, p + s)
+            slots.append(wl.block_tables[r, j // 16].astype(np.int64) * 16 + j % 16)
+        slots = torch.from_numpy(np.concatenate(slots).astype(np.int32)).to(dev)
+        t = slots.numel()
+        k_new = torch.randn((t, hkv, d), device=dev).to(torch.bfloat16)
+        v_new = torch.randn((t, hkv, d), device=dev).to(torch.bfloat16)
+        moved = 2 * 2 * t * hkv * d * 2        # K and V, read once and written once
+
+        def fn():
+            ops.cs_kv_write(k_new, v_new, slots, k_pool, v_pool, stream=stream)
+        peak, bound, unit_desc = PEAK_HBM_GBS, "hbm", f"{t} tokens"
+    else:
+        n = 256
+        ids = torch.from_numpy(np.random.default_rng(5).choice(wl.num_blocks, n, replace=False)
+                               .astype(np.int32)).to(dev)
+        host_k = torch.empty((n, hkv, 16, d), dtype=torch.bfloat16, pin_memory=True)
+        host_v = torch.empty_like(host_k, pin_memory=True)
+        moved = 2 * n * hkv * 16 * d * 2        # K and V blocks over the host link
+
+        def fn():
+            ops.cs_kv_offload(ids, k_pool, v_pool, host_k, host_v, stream=stream)
+        peak, bound, unit_desc = PEAK_PCIE5_X16_GBS, "host_link", f"{n} blocks"
+    wall, avg_ms = _time_launches(fn, args.steps, args.warmup, stream)
+    gbs = moved / (avg_ms * 1e-3) / 1e9
+    return {"metric": f"{args.component} GB/s, 1 MI355X", "value": round(gbs, 2), "unit": "GB/s",
+            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": round(wall / args.steps * 1e3, 4), "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"{args.component} of {unit_desc} of {args.workload}",
+                       "bytes_per_launch": moved},
+            "roofline": {"bound": bound, "achieved": round(gbs, 2), "peak": peak, "unit": "GB/s",
+                         "frac": round(gbs / peak, 4), "traffic": None,
+                         "avg_launch_us": round(avg_ms * 1e3, 2)},
+            "cpu_baseline": None}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +184,10 @@ def main():
     ap.add_argument("--workload", default="llama70b_prefetch",
                     choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--component", default="pipeline",
+                    choices=("pipeline", "kv_write", "kv_offload"),
+                    help="pipeline (default): the serving step; kv_write / kv_offload: "
+                         "the write-back scatter and the offload copy on their own")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a plain 1 GiB device-to-device copy (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -141,6 +214,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes_read": nbytes, "copy_probe_bytes_written": nbytes,
                           "launches": 5}), flush=True)
+        return
+    if args.component != "pipeline":
+        print(json.dumps(bench_copy(args, dev)), flush=True)
         return
     wl = make_config(args.workload)
     dw = pipeline.DeviceWorkload(wl, dev)

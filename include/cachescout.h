@@ -2,9 +2,9 @@
  * cachescout.h - C ABI of libcachescout.so: paged prefix-reuse prefill
  * attention and KV prefetch for AMD Instinct MI355X (gfx950).
  *
- * The two calls are the GPU work behind agent-aware KV-cache reuse
- * (arXiv 2608.14624, "Learning Agent Execution for KV-Cache Management in
- * Agentic Serving"):
+ * The calls are the GPU work behind agent-aware KV-cache reuse (arXiv
+ * 2608.14624, "Learning Agent Execution for KV-Cache Management in Agentic
+ * Serving"):
  *
  *   cs_prefill_paged_attn  - an agent invocation that hits its cached prompt
  *                            prefix (the "agent anchor", Sec. 2.1) runs
@@ -18,13 +18,18 @@
  *                            reloaded from the CPU tier into free pool slots
  *                            (architecture figure of Sec. 3; Sec. 4), as a
  *                            bit-exact block copy.
+ *   cs_kv_write            - the K/V of new tokens is stored into pool slots
+ *                            through a slot mapping (the write that precedes
+ *                            attention, Sec. 2.1 and Sec. 4).
+ *   cs_kv_offload          - whole blocks are copied from the pool to the
+ *                            CPU tier (Sec. 4), the reverse of the prefetch.
  *
- * Conventions shared by both calls
+ * Conventions shared by all calls
  *   - Every pointer is caller-owned.  The library allocates no device or host
  *     memory and keeps no state beyond a per-process cache of device
  *     properties; calls are reentrant and may run concurrently on different
  *     streams.
- *   - Both calls enqueue their kernel on `stream` (NULL = the legacy default
+ *   - Every call enqueues its kernel on `stream` (NULL = the legacy default
  *     stream of the current device) and return without synchronizing.  Device
  *     metadata is read by the kernels, never by the host, so the calls can be
  *     captured in a HIP graph (unless CS_DEBUG_CHECK=1, see below).
@@ -152,6 +157,56 @@ int cs_kv_prefetch(const void *host_k_blocks, const void *host_v_blocks,
                    const int32_t *dst_block_ids, int32_t n, void *k_pool, void *v_pool,
                    int32_t num_blocks, int32_t num_kv_heads, int32_t head_dim,
                    int32_t block_size, cs_stream_t stream);
+
+/*
+ * KV write-back: store the K/V rows of new tokens into their pool slots.
+ *
+ * Operation (Sec. 2.1: prefill computes the KV of every prompt token and the
+ * prefix cache keeps it in 16-token blocks; Sec. 4: a warmup produces the
+ * same KV blocks as a normal invocation): for every token t < num_tokens with
+ * s = slot_mapping[t] >= 0 and every KV head h,
+ *   k_pool[s / block_size][h][s % block_size][:] = k_new[t][h][:]
+ *   v_pool[s / block_size][h][s % block_size][:] = v_new[t][h][:]
+ * byte for byte.  Tokens with a negative slot are skipped.  This is the
+ * write that puts a suffix's own K/V into the pool before
+ * cs_prefill_paged_attn reads it.
+ *
+ * Arguments
+ *   k_new, v_new   device, bf16 [num_tokens][num_kv_heads][head_dim], 16-byte
+ *                  aligned.
+ *   slot_mapping   device, int32 [num_tokens]; the non-negative entries are
+ *                  distinct and < num_blocks * block_size.
+ *   k_pool, v_pool device, as in cs_prefill_paged_attn.
+ *   num_tokens == 0 is a no-op returning CS_OK.
+ */
+int cs_kv_write(const void *k_new, const void *v_new, const int32_t *slot_mapping,
+                int32_t num_tokens, void *k_pool, void *v_pool, int32_t num_blocks,
+                int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                cs_stream_t stream);
+
+/*
+ * KV offload: copy whole pool blocks to pinned host memory.
+ *
+ * Operation (Sec. 4: blocks are kept in the CPU tier, and eviction prefers
+ * blocks already resident there; the reverse of cs_kv_prefetch): for every
+ * i < n, host_k_blocks[i] = k_pool[src_block_ids[i]] and host_v_blocks[i] =
+ * v_pool[src_block_ids[i]], byte for byte.  The kernel writes the host
+ * buffers directly over the host link.
+ *
+ * Arguments
+ *   src_block_ids  device, int32 [n], each in [0, num_blocks) (repeats allowed).
+ *   k_pool, v_pool device, as in cs_prefill_paged_attn.
+ *   host_k_blocks,
+ *   host_v_blocks  pinned, device-mapped host memory, bf16
+ *                  [n][num_kv_heads][block_size][head_dim], 16-byte aligned;
+ *                  anything else -> CS_ERR_INVALID_ARG.  Read them only after
+ *                  the stream has passed this call.
+ *   n == 0 is a no-op returning CS_OK.
+ */
+int cs_kv_offload(const int32_t *src_block_ids, int32_t n, const void *k_pool,
+                  const void *v_pool, int32_t num_blocks, void *host_k_blocks,
+                  void *host_v_blocks, int32_t num_kv_heads, int32_t head_dim,
+                  int32_t block_size, cs_stream_t stream);
 
 /* Static, NUL-terminated name of a status code ("CS_OK", ...). */
 const char *cs_status_string(int status);

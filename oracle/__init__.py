@@ -29,7 +29,9 @@ attention oracle is the plain definition of scaled dot-product attention with
 a causal mask aligned to the end of the prompt, evaluated in float64
 (``paged_attention.py``), pinned by a scalar brute force (``brute.py``) and by
 the invariants and closed forms in ``tests/test_oracle_*.py``.  The prefetch
-oracle is a NumPy scatter (``prefetch.py``).
+oracle is a NumPy scatter (``prefetch.py``); the write-back of new tokens'
+K/V through a slot mapping and the offload of blocks to the CPU tier are
+NumPy scatters and gathers too (``kv_copy.py``).
 
 Every function here is pinned; none is "parity unpinned".
 """
@@ -43,4 +45,5 @@ from .paged_attention import (  # noqa: F401
     visible_keys,
 )
 from .prefetch import kv_prefetch  # noqa: F401
+from .kv_copy import kv_offload, kv_write  # noqa: F401
 from .brute import brute_attention_rows  # noqa: F401

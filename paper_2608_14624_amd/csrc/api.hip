@@ -93,6 +93,31 @@ int debug_check_prefetch(const int32_t* dst, int n, int num_blocks, hipStream_t 
   return CS_OK;
 }
 
+int debug_check_slots(const int32_t* slots, int n, long long num_slots, hipStream_t stream) {
+  std::vector<int32_t> ids;
+  hipError_t e = copy_to_host(ids, slots, (size_t)n, stream);
+  if (e != hipSuccess) return hip_fail(e, "CS_DEBUG_CHECK metadata copy");
+  std::vector<unsigned char> seen((size_t)num_slots, 0);
+  for (int i = 0; i < n; ++i) {
+    if (ids[i] < 0) continue;
+    if (ids[i] >= num_slots)
+      return fail(CS_ERR_INVALID_ARG, "slot_mapping[%d] = %d outside [0, %lld)", i, ids[i], num_slots);
+    if (seen[ids[i]]) return fail(CS_ERR_INVALID_ARG, "slot_mapping[%d] = %d is a duplicate", i, ids[i]);
+    seen[ids[i]] = 1;
+  }
+  return CS_OK;
+}
+
+int debug_check_block_ids(const int32_t* ids_d, int n, int num_blocks, hipStream_t stream) {
+  std::vector<int32_t> ids;
+  hipError_t e = copy_to_host(ids, ids_d, (size_t)n, stream);
+  if (e != hipSuccess) return hip_fail(e, "CS_DEBUG_CHECK metadata copy");
+  for (int i = 0; i < n; ++i)
+    if (ids[i] < 0 || ids[i] >= num_blocks)
+      return fail(CS_ERR_INVALID_ARG, "src_block_ids[%d] = %d outside [0, %d)", i, ids[i], num_blocks);
+  return CS_OK;
+}
+
 // Device-visible address of a pinned, device-mapped host buffer, or null.
 const void* mapped_host_pointer(const void* host, const char* name, int* status) {
   hipPointerAttribute_t attr;
@@ -224,6 +249,80 @@ int cs_kv_prefetch(const void* host_k_blocks, const void* host_v_blocks,
   a.block_bytes = (long long)num_kv_heads * block_size * head_dim * 2;
   hipError_t e = cs::launch_kv_prefetch(a, s);
   if (e != hipSuccess) return hip_fail(e, "kv_prefetch launch");
+  return ok();
+}
+
+int cs_kv_write(const void* k_new, const void* v_new, const int32_t* slot_mapping,
+                int32_t num_tokens, void* k_pool, void* v_pool, int32_t num_blocks,
+                int32_t num_kv_heads, int32_t head_dim, int32_t block_size, cs_stream_t stream) {
+  if (num_tokens < 0 || num_blocks < 0) return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+    return fail(CS_ERR_INVALID_ARG, "num_kv_heads, head_dim and block_size must be positive");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
+  if (num_tokens == 0) return ok();
+  if (!k_new || !v_new || !slot_mapping || !k_pool || !v_pool)
+    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  if (num_blocks == 0) return fail(CS_ERR_INVALID_ARG, "num_blocks is 0");
+  if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pool) || !aligned16(v_pool))
+    return fail(CS_ERR_INVALID_ARG, "k_new, v_new and the pools must be 16-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (debug_checks_enabled()) {
+    int st = debug_check_slots(slot_mapping, num_tokens, (long long)num_blocks * block_size, s);
+    if (st != CS_OK) return st;
+  }
+  cs::KvWriteLaunch a;
+  a.k_new = static_cast<const uint16_t*>(k_new);
+  a.v_new = static_cast<const uint16_t*>(v_new);
+  a.slot_mapping = slot_mapping;
+  a.num_tokens = num_tokens;
+  a.k_pool = static_cast<uint16_t*>(k_pool);
+  a.v_pool = static_cast<uint16_t*>(v_pool);
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.block_size = block_size;
+  hipError_t e = cs::launch_kv_write(a, s);
+  if (e != hipSuccess) return hip_fail(e, "kv_write launch");
+  return ok();
+}
+
+int cs_kv_offload(const int32_t* src_block_ids, int32_t n, const void* k_pool, const void* v_pool,
+                  int32_t num_blocks, void* host_k_blocks, void* host_v_blocks,
+                  int32_t num_kv_heads, int32_t head_dim, int32_t block_size, cs_stream_t stream) {
+  if (n < 0 || num_blocks < 0) return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+    return fail(CS_ERR_INVALID_ARG, "num_kv_heads, head_dim and block_size must be positive");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
+  if (n == 0) return ok();
+  if (!src_block_ids || !k_pool || !v_pool || !host_k_blocks || !host_v_blocks)
+    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  if (num_blocks == 0) return fail(CS_ERR_INVALID_ARG, "num_blocks is 0");
+  if (!aligned16(host_k_blocks) || !aligned16(host_v_blocks) || !aligned16(k_pool) ||
+      !aligned16(v_pool))
+    return fail(CS_ERR_INVALID_ARG, "host buffers and pools must be 16-byte aligned");
+  int st = CS_OK;
+  const void* dk = mapped_host_pointer(host_k_blocks, "host_k_blocks", &st);
+  if (st != CS_OK) return st;
+  const void* dv = mapped_host_pointer(host_v_blocks, "host_v_blocks", &st);
+  if (st != CS_OK) return st;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (debug_checks_enabled()) {
+    st = debug_check_block_ids(src_block_ids, n, num_blocks, s);
+    if (st != CS_OK) return st;
+  }
+  cs::KvOffloadLaunch a;
+  a.src_ids = src_block_ids;
+  a.n = n;
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.host_k = const_cast<uint16_t*>(static_cast<const uint16_t*>(dk));
+  a.host_v = const_cast<uint16_t*>(static_cast<const uint16_t*>(dv));
+  a.block_bytes = (long long)num_kv_heads * block_size * head_dim * 2;
+  hipError_t e = cs::launch_kv_offload(a, s);
+  if (e != hipSuccess) return hip_fail(e, "kv_offload launch");
   return ok();
 }
 

@@ -48,4 +48,30 @@ struct PrefetchLaunch {
 
 hipError_t launch_kv_prefetch(const PrefetchLaunch& a, hipStream_t stream);
 
+struct KvWriteLaunch {
+  const uint16_t* k_new;    // [num_tokens][num_kv_heads][head_dim]
+  const uint16_t* v_new;
+  const int32_t* slot_mapping;
+  int num_tokens;
+  uint16_t* k_pool;
+  uint16_t* v_pool;
+  int num_kv_heads;
+  int head_dim;
+  int block_size;
+};
+
+hipError_t launch_kv_write(const KvWriteLaunch& a, hipStream_t stream);
+
+struct KvOffloadLaunch {
+  const int32_t* src_ids;
+  int n;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  uint16_t* host_k;         // device-visible addresses of the pinned host buffers
+  uint16_t* host_v;
+  long long block_bytes;
+};
+
+hipError_t launch_kv_offload(const KvOffloadLaunch& a, hipStream_t stream);
+
 }  // namespace cs

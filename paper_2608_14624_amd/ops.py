@@ -20,7 +20,8 @@ CS_ERR_UNSUPPORTED = 2
 CS_ERR_HIP = 3
 
 # every symbol the C header declares
-EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_status_string", "cs_last_error")
+EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_kv_write", "cs_kv_offload",
+            "cs_status_string", "cs_last_error")
 
 
 class CacheScoutError(RuntimeError):
@@ -41,6 +42,10 @@ def _load():
     lib.cs_prefill_paged_attn.restype = ctypes.c_int
     lib.cs_kv_prefetch.argtypes = [vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp]
     lib.cs_kv_prefetch.restype = ctypes.c_int
+    lib.cs_kv_write.argtypes = [vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp]
+    lib.cs_kv_write.restype = ctypes.c_int
+    lib.cs_kv_offload.argtypes = [vp, i32, vp, vp, i32, vp, vp, i32, i32, i32, vp]
+    lib.cs_kv_offload.restype = ctypes.c_int
     lib.cs_status_string.argtypes = [ctypes.c_int]
     lib.cs_status_string.restype = ctypes.c_char_p
     lib.cs_last_error.argtypes = []
@@ -166,3 +171,62 @@ def cs_kv_prefetch(host_k, host_v, dst_block_ids, k_pool, v_pool, *, stream=None
                                 _ptr(k_pool), _ptr(v_pool), num_blocks, hkv, d, bs,
                                 _stream_handle(stream, dev))
     _check(status)
+
+
+def cs_kv_write_raw(k_new, v_new, slot_mapping, num_tokens, k_pool, v_pool, num_blocks,
+                    num_kv_heads, head_dim, block_size, stream=0):
+    """The C call with raw pointers (ints or None); returns the status code."""
+    return _lib.cs_kv_write(k_new, v_new, slot_mapping, num_tokens, k_pool, v_pool, num_blocks,
+                            num_kv_heads, head_dim, block_size, stream)
+
+
+def cs_kv_offload_raw(src_block_ids, n, k_pool, v_pool, num_blocks, host_k, host_v,
+                      num_kv_heads, head_dim, block_size, stream=0):
+    """The C call with raw pointers (ints or None); returns the status code."""
+    return _lib.cs_kv_offload(src_block_ids, n, k_pool, v_pool, num_blocks, host_k, host_v,
+                              num_kv_heads, head_dim, block_size, stream)
+
+
+def cs_kv_write(k_new, v_new, slot_mapping, k_pool, v_pool, *, stream=None):
+    """Enqueue the write of new tokens' K/V into their pool slots.
+
+    ``k_new``/``v_new``: bf16 GPU tensors ``[T, Hkv, D]``; ``slot_mapping``:
+    int32 GPU tensor ``[T]`` (block * 16 + offset, negative = skip); pools as
+    for attention.
+    """
+    dev = k_pool.device
+    for name, t, dt in (("k_new", k_new, torch.bfloat16), ("v_new", v_new, torch.bfloat16),
+                        ("slot_mapping", slot_mapping, torch.int32),
+                        ("k_pool", k_pool, torch.bfloat16), ("v_pool", v_pool, torch.bfloat16)):
+        _require(t.is_cuda and t.device == dev, f"{name} must be on {dev}")
+        _require(t.dtype == dt, f"{name} must be {dt}")
+        _require(t.is_contiguous(), f"{name} must be contiguous")
+    _require(k_new.shape == v_new.shape and k_new.dim() == 3, "k_new/v_new must be [T, Hkv, D]")
+    _require(k_pool.shape == v_pool.shape, "pools must match")
+    num_blocks, hkv, bs, d = k_pool.shape
+    _require(tuple(k_new.shape[1:]) == (hkv, d), "token rows must match the pool's heads and dims")
+    n = k_new.shape[0]
+    _require(slot_mapping.numel() == n, "slot_mapping must have one entry per token")
+    _check(cs_kv_write_raw(_ptr(k_new), _ptr(v_new), _ptr(slot_mapping), n, _ptr(k_pool),
+                           _ptr(v_pool), num_blocks, hkv, d, bs, _stream_handle(stream, dev)))
+
+
+def cs_kv_offload(src_block_ids, k_pool, v_pool, host_k, host_v, *, stream=None):
+    """Enqueue the copy of pool blocks ``src_block_ids`` into pinned host buffers."""
+    dev = k_pool.device
+    _require(host_k.device.type == "cpu" and host_v.device.type == "cpu",
+             "host blocks must be CPU tensors")
+    _require(host_k.is_pinned() and host_v.is_pinned(), "host blocks must be pinned")
+    _require(host_k.dtype == torch.bfloat16 and host_v.dtype == torch.bfloat16,
+             "host blocks must be bf16")
+    _require(host_k.is_contiguous() and host_v.is_contiguous(), "host blocks must be contiguous")
+    _require(src_block_ids.dtype == torch.int32 and src_block_ids.device == dev,
+             "src_block_ids must be int32 on the pool's device")
+    _require(k_pool.shape == v_pool.shape and k_pool.dtype == torch.bfloat16,
+             "pools must match and be bf16")
+    n = src_block_ids.numel()
+    _require(host_k.shape[0] >= n and host_v.shape[0] >= n, "fewer host blocks than ids")
+    _require(tuple(host_k.shape[1:]) == tuple(k_pool.shape[1:]), "host block shape != pool block shape")
+    num_blocks, hkv, bs, d = k_pool.shape
+    _check(cs_kv_offload_raw(_ptr(src_block_ids), n, _ptr(k_pool), _ptr(v_pool), num_blocks,
+                             _ptr(host_k), _ptr(host_v), hkv, d, bs, _stream_handle(stream, dev)))

@@ -112,3 +112,48 @@ def test_prefetch_rejects_bad_arguments(kw, status):
 
 def test_prefetch_zero_blocks_is_a_noop():
     assert prefetch(n=0, host_k=None, host_v=None) == ops.CS_OK
+
+
+WGOOD = dict(k_new=FAKE, v_new=FAKE, slot_mapping=FAKE, num_tokens=10, k_pool=FAKE, v_pool=FAKE,
+             num_blocks=64, num_kv_heads=2, head_dim=128, block_size=16, stream=0)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(num_tokens=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(head_dim=32), ops.CS_ERR_UNSUPPORTED),
+    (dict(block_size=32), ops.CS_ERR_UNSUPPORTED),
+    (dict(k_new=None), ops.CS_ERR_INVALID_ARG),
+    (dict(slot_mapping=None), ops.CS_ERR_INVALID_ARG),
+    (dict(num_blocks=0), ops.CS_ERR_INVALID_ARG),
+    (dict(v_pool=FAKE + 2), ops.CS_ERR_INVALID_ARG),
+])
+def test_kv_write_rejects_bad_arguments(kw, status):
+    args = dict(WGOOD)
+    args.update(kw)
+    assert ops.cs_kv_write_raw(**args) == status
+
+
+def test_kv_write_zero_tokens_is_a_noop():
+    args = dict(WGOOD, num_tokens=0, k_new=None)
+    assert ops.cs_kv_write_raw(**args) == ops.CS_OK
+
+
+OGOOD = dict(src_block_ids=FAKE, n=4, k_pool=FAKE, v_pool=FAKE, num_blocks=64, host_k=FAKE,
+             host_v=FAKE, num_kv_heads=2, head_dim=64, block_size=16, stream=0)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(head_dim=96), ops.CS_ERR_UNSUPPORTED),
+    (dict(host_k=None), ops.CS_ERR_INVALID_ARG),
+    (dict(src_block_ids=None), ops.CS_ERR_INVALID_ARG),
+    (dict(host_v=FAKE + 4), ops.CS_ERR_INVALID_ARG),
+])
+def test_kv_offload_rejects_bad_arguments(kw, status):
+    args = dict(OGOOD)
+    args.update(kw)
+    assert ops.cs_kv_offload_raw(**args) == status
+
+
+def test_kv_offload_zero_blocks_is_a_noop():
+    assert ops.cs_kv_offload_raw(**dict(OGOOD, n=0, host_k=None)) == ops.CS_OK
