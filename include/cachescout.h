@@ -23,6 +23,8 @@
  *                            attention, Sec. 2.1 and Sec. 4).
  *   cs_kv_offload          - whole blocks are copied from the pool to the
  *                            CPU tier (Sec. 4), the reverse of the prefetch.
+ *   cs_paged_decode_attn   - one new token per sequence attends over its whole
+ *                            paged KV (the decode that follows a prefill).
  *
  * Conventions shared by all calls
  *   - Every pointer is caller-owned.  The library allocates no device or host
@@ -65,7 +67,8 @@ enum cs_status {
                                 sizes, misaligned buffer, non-pinned host
                                 buffer, or (debug mode) bad device metadata */
     CS_ERR_UNSUPPORTED = 2,  /* valid but not implemented: head_dim other
-                                than 64 or 128, block_size other than 16 */
+                                than 64 or 128, block_size other than 16,
+                                more than 16 query heads per KV head (decode) */
     CS_ERR_HIP = 3           /* the HIP runtime reported an error */
 };
 
@@ -157,6 +160,31 @@ int cs_kv_prefetch(const void *host_k_blocks, const void *host_v_blocks,
                    const int32_t *dst_block_ids, int32_t n, void *k_pool, void *v_pool,
                    int32_t num_blocks, int32_t num_kv_heads, int32_t head_dim,
                    int32_t block_size, cs_stream_t stream);
+
+/*
+ * Paged decode attention: one query token per sequence over all its keys.
+ *
+ * Operation (the one-token case of cs_prefill_paged_attn, i.e. P = L - 1,
+ * S = 1: the per-turn latency of Sec. 5 includes the decode that follows
+ * the prefill): for every sequence r < batch, query head h and d,
+ *   L = seq_lens[r],  g = h / (num_q_heads / num_kv_heads)
+ *   out[r][h][d] = sum_{j < L} softmax_j(scale * dot(q[r][h], K_r[j])) V_r[j][d]
+ * with K_r, V_r read through block_tables as in cs_prefill_paged_attn.  The
+ * token's own K/V must already be in the pool (cs_kv_write).  Same
+ * arithmetic conventions as cs_prefill_paged_attn.
+ *
+ * Arguments
+ *   q, out         device, bf16 [batch][num_q_heads][head_dim], 16-byte aligned.
+ *   block_tables   device, int32 [batch][max_blocks_per_seq].
+ *   seq_lens       device, int32 [batch], each in [1, max_seq_len].
+ *   num_q_heads / num_kv_heads <= 16; head_dim 64 or 128; block_size 16.
+ *   batch == 0 is a no-op returning CS_OK.
+ */
+int cs_paged_decode_attn(const void *q, const void *k_pool, const void *v_pool,
+                         const int32_t *block_tables, const int32_t *seq_lens, int32_t batch,
+                         int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
+                         int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                         int32_t block_size, float scale, void *out, cs_stream_t stream);
 
 /*
  * KV write-back: store the K/V rows of new tokens into their pool slots.

@@ -118,6 +118,25 @@ int debug_check_block_ids(const int32_t* ids_d, int n, int num_blocks, hipStream
   return CS_OK;
 }
 
+int debug_check_decode(const int32_t* block_tables, const int32_t* seq_lens, int batch,
+                       int max_seq_len, int max_blocks_per_seq, int num_blocks,
+                       hipStream_t stream) {
+  std::vector<int32_t> sl, bt;
+  hipError_t e = copy_to_host(sl, seq_lens, (size_t)batch, stream);
+  if (e == hipSuccess) e = copy_to_host(bt, block_tables, (size_t)batch * max_blocks_per_seq, stream);
+  if (e != hipSuccess) return hip_fail(e, "CS_DEBUG_CHECK metadata copy");
+  for (int r = 0; r < batch; ++r) {
+    if (sl[r] < 1 || sl[r] > max_seq_len)
+      return fail(CS_ERR_INVALID_ARG, "seq_lens[%d] = %d outside [1, %d]", r, sl[r], max_seq_len);
+    for (int b = 0; b < (sl[r] + 15) / 16; ++b) {
+      const int32_t slot = bt[(size_t)r * max_blocks_per_seq + b];
+      if (slot < 0 || slot >= num_blocks)
+        return fail(CS_ERR_INVALID_ARG, "block_tables[%d][%d] = %d outside [0, %d)", r, b, slot, num_blocks);
+    }
+  }
+  return CS_OK;
+}
+
 // Device-visible address of a pinned, device-mapped host buffer, or null.
 const void* mapped_host_pointer(const void* host, const char* name, int* status) {
   hipPointerAttribute_t attr;
@@ -249,6 +268,58 @@ int cs_kv_prefetch(const void* host_k_blocks, const void* host_v_blocks,
   a.block_bytes = (long long)num_kv_heads * block_size * head_dim * 2;
   hipError_t e = cs::launch_kv_prefetch(a, s);
   if (e != hipSuccess) return hip_fail(e, "kv_prefetch launch");
+  return ok();
+}
+
+int cs_paged_decode_attn(const void* q, const void* k_pool, const void* v_pool,
+                         const int32_t* block_tables, const int32_t* seq_lens, int32_t batch,
+                         int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
+                         int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                         int32_t block_size, float scale, void* out, cs_stream_t stream) {
+  if (batch < 0 || max_seq_len < 0 || max_blocks_per_seq < 0 || num_blocks < 0)
+    return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+    return fail(CS_ERR_INVALID_ARG, "head counts, head_dim and block_size must be positive");
+  if (num_q_heads % num_kv_heads != 0)
+    return fail(CS_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                num_q_heads, num_kv_heads);
+  if (num_q_heads / num_kv_heads > 16)
+    return fail(CS_ERR_UNSUPPORTED, "more than 16 query heads per KV head");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
+  if (!isfinite(scale)) return fail(CS_ERR_INVALID_ARG, "scale is not finite");
+  if (batch == 0) return ok();
+  if (!q || !k_pool || !v_pool || !block_tables || !seq_lens || !out)
+    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  if (num_blocks == 0 || max_seq_len == 0)
+    return fail(CS_ERR_INVALID_ARG, "num_blocks and max_seq_len must be positive");
+  if ((long long)max_blocks_per_seq * block_size < max_seq_len)
+    return fail(CS_ERR_INVALID_ARG, "max_blocks_per_seq * block_size < max_seq_len");
+  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool))
+    return fail(CS_ERR_INVALID_ARG, "q, k_pool and v_pool must be 16-byte aligned");
+  if ((long long)batch * num_kv_heads > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (debug_checks_enabled()) {
+    int st = debug_check_decode(block_tables, seq_lens, batch, max_seq_len, max_blocks_per_seq,
+                                num_blocks, s);
+    if (st != CS_OK) return st;
+  }
+  cs::DecodeLaunch a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_tables = block_tables;
+  a.seq_lens = seq_lens;
+  a.out = static_cast<uint16_t*>(out);
+  a.batch = batch;
+  a.max_blocks_per_seq = max_blocks_per_seq;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.scale = scale;
+  hipError_t e = cs::launch_paged_decode_attn(a, s);
+  if (e != hipSuccess) return hip_fail(e, "paged_decode_attn launch");
   return ok();
 }
 

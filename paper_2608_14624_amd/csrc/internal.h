@@ -74,4 +74,21 @@ struct KvOffloadLaunch {
 
 hipError_t launch_kv_offload(const KvOffloadLaunch& a, hipStream_t stream);
 
+struct DecodeLaunch {
+  const uint16_t* q;        // [batch][num_q_heads][head_dim]
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_tables;
+  const int32_t* seq_lens;
+  uint16_t* out;
+  int batch;
+  int max_blocks_per_seq;
+  int num_q_heads;
+  int num_kv_heads;
+  int head_dim;
+  float scale;
+};
+
+hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream);
+
 }  // namespace cs

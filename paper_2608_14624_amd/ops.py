@@ -21,7 +21,7 @@ CS_ERR_HIP = 3
 
 # every symbol the C header declares
 EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_kv_write", "cs_kv_offload",
-            "cs_status_string", "cs_last_error")
+            "cs_paged_decode_attn", "cs_status_string", "cs_last_error")
 
 
 class CacheScoutError(RuntimeError):
@@ -46,6 +46,9 @@ def _load():
     lib.cs_kv_write.restype = ctypes.c_int
     lib.cs_kv_offload.argtypes = [vp, i32, vp, vp, i32, vp, vp, i32, i32, i32, vp]
     lib.cs_kv_offload.restype = ctypes.c_int
+    lib.cs_paged_decode_attn.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32,
+                                         i32, f32, vp, vp]
+    lib.cs_paged_decode_attn.restype = ctypes.c_int
     lib.cs_status_string.argtypes = [ctypes.c_int]
     lib.cs_status_string.restype = ctypes.c_char_p
     lib.cs_last_error.argtypes = []
@@ -230,3 +233,38 @@ def cs_kv_offload(src_block_ids, k_pool, v_pool, host_k, host_v, *, stream=None)
     num_blocks, hkv, bs, d = k_pool.shape
     _check(cs_kv_offload_raw(_ptr(src_block_ids), n, _ptr(k_pool), _ptr(v_pool), num_blocks,
                              _ptr(host_k), _ptr(host_v), hkv, d, bs, _stream_handle(stream, dev)))
+
+
+def cs_paged_decode_attn_raw(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
+                             max_blocks_per_seq, num_blocks, num_q_heads, num_kv_heads, head_dim,
+                             block_size, scale, out, stream=0):
+    """The C call with raw pointers (ints or None); returns the status code."""
+    return _lib.cs_paged_decode_attn(q, k_pool, v_pool, block_tables, seq_lens, batch,
+                                     max_seq_len, max_blocks_per_seq, num_blocks, num_q_heads,
+                                     num_kv_heads, head_dim, block_size, ctypes.c_float(scale),
+                                     out, stream)
+
+
+def cs_paged_decode_attn(q, k_pool, v_pool, block_tables, seq_lens, out, *, max_seq_len, scale,
+                         stream=None):
+    """Enqueue paged decode attention: ``q``/``out`` bf16 ``[B, Hq, D]``,
+    ``seq_lens`` int32 ``[B]``, pools and block tables as for prefill."""
+    dev = q.device
+    for name, t, dt in (("q", q, torch.bfloat16), ("k_pool", k_pool, torch.bfloat16),
+                        ("v_pool", v_pool, torch.bfloat16), ("out", out, torch.bfloat16),
+                        ("block_tables", block_tables, torch.int32),
+                        ("seq_lens", seq_lens, torch.int32)):
+        _require(t.is_cuda and t.device == dev, f"{name} must be on {dev}")
+        _require(t.dtype == dt, f"{name} must be {dt}")
+        _require(t.is_contiguous(), f"{name} must be contiguous")
+    _require(q.dim() == 3 and out.shape == q.shape, "q and out must be [B, Hq, D]")
+    _require(k_pool.shape == v_pool.shape and k_pool.dim() == 4, "pools must match")
+    batch, hq, d = q.shape
+    num_blocks, hkv, bs, d2 = k_pool.shape
+    _require(d == d2, "head_dim of q and pools differ")
+    _require(block_tables.dim() == 2 and block_tables.shape[0] == batch, "block_tables must be [B, max_blocks]")
+    _require(seq_lens.numel() == batch, "seq_lens must have B entries")
+    _check(cs_paged_decode_attn_raw(_ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_tables),
+                                    _ptr(seq_lens), batch, int(max_seq_len), block_tables.shape[1],
+                                    num_blocks, hq, hkv, d, bs, float(scale), _ptr(out),
+                                    _stream_handle(stream, dev)))

@@ -373,7 +373,8 @@ def _anchor_share(anchor_lens, invs):
 # The named configurations
 # --------------------------------------------------------------------------
 
-CONFIG_NAMES = ("tiny", "llama8b", "agent_batch", "llama70b_prefetch", "long_mixed")
+CONFIG_NAMES = ("tiny", "llama8b", "agent_batch", "llama70b_prefetch", "long_mixed",
+                "decode_batch")
 
 
 def config_spec(name):
@@ -420,7 +421,30 @@ def config_spec(name):
         invs = [Invocation(int(a), int(s), bool(h)) for a, s, h in zip(agents, sfx, hits)]
         return dict(seed=4, anchor_lens=anchors, invocations=invs,
                     num_q_heads=32, num_kv_heads=8, head_dim=128, occupancy=0.9)
+    if name == "decode_batch":
+        # decode after the agent turns: 128 sequences over 8 agents, each the
+        # agent's anchor U[4096, 8192] + its own history (lognormal, median
+        # 512, clipped to [128, 4096]) ending in the token being decoded
+        rng = np.random.default_rng([5, _K_SPEC])
+        anchors = [int(x) for x in rng.integers(4096, 8192, size=8, endpoint=True)]
+        agents = rng.integers(0, 8, size=128)
+        hist = np.clip(np.rint(rng.lognormal(np.log(512.0), 1.0, size=128)), 128, 4096)
+        invs = [Invocation(int(a), int(s)) for a, s in zip(agents, hist)]
+        return dict(seed=5, anchor_lens=anchors, invocations=invs,
+                    num_q_heads=32, num_kv_heads=8, head_dim=128, occupancy=0.9)
     raise KeyError(name)
+
+
+def decode_view(wl):
+    """The last suffix token of every invocation as a decode batch.
+
+    Returns ``(q [B, Hq, D], seq_lens [B])``: row ``r`` is the query of the
+    last prompt position of invocation ``r``, which sees all ``P_r + S_r``
+    keys.  The pools and block tables of ``wl`` serve unchanged.
+    """
+    last = wl.cu_q_lens[1:].astype(np.int64) - 1
+    assert np.all(wl.q_lens > 0), "every invocation needs a token to decode"
+    return np.ascontiguousarray(wl.q[last]), wl.kv_lens.astype(np.int32)
 
 
 def make_config(name):

@@ -157,3 +157,28 @@ def test_kv_offload_rejects_bad_arguments(kw, status):
 
 def test_kv_offload_zero_blocks_is_a_noop():
     assert ops.cs_kv_offload_raw(**dict(OGOOD, n=0, host_k=None)) == ops.CS_OK
+
+
+DGOOD = dict(q=FAKE, k_pool=FAKE, v_pool=FAKE, block_tables=FAKE, seq_lens=FAKE, batch=4,
+             max_seq_len=100, max_blocks_per_seq=7, num_blocks=64, num_q_heads=8, num_kv_heads=2,
+             head_dim=128, block_size=16, scale=0.1, out=FAKE, stream=0)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(num_q_heads=64, num_kv_heads=2), ops.CS_ERR_UNSUPPORTED),   # 32 heads per KV head
+    (dict(num_kv_heads=3), ops.CS_ERR_INVALID_ARG),
+    (dict(head_dim=80), ops.CS_ERR_UNSUPPORTED),
+    (dict(q=None), ops.CS_ERR_INVALID_ARG),
+    (dict(max_blocks_per_seq=6), ops.CS_ERR_INVALID_ARG),             # 96 < 100
+    (dict(max_seq_len=0), ops.CS_ERR_INVALID_ARG),
+    (dict(scale=float("inf")), ops.CS_ERR_INVALID_ARG),
+])
+def test_decode_rejects_bad_arguments(kw, status):
+    args = dict(DGOOD)
+    args.update(kw)
+    assert ops.cs_paged_decode_attn_raw(**args) == status
+
+
+def test_decode_empty_batch_is_a_noop():
+    assert ops.cs_paged_decode_attn_raw(**dict(DGOOD, batch=0, q=None)) == ops.CS_OK
