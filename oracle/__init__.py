@@ -33,6 +33,12 @@ oracle is a NumPy scatter (``prefetch.py``); the write-back of new tokens'
 K/V through a slot mapping and the offload of blocks to the CPU tier are
 NumPy scatters and gathers too (``kv_copy.py``).
 
+The host-side control plane (Sec. 3.2-3.4, Eq. (2)-(11), the runtime
+workflow algorithm) is plain Python in ``control_plane.py``, pinned by hand
+values, closed forms, breadth-first distances against all-pairs shortest
+paths, the exact survival probability by path enumeration, and planted
+mistakes (``tests/test_control_plane_oracle.py``).
+
 Every function here is pinned; none is "parity unpinned".
 """
 

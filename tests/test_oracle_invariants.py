@@ -151,9 +151,9 @@ def test_closed_form_dominant_key():
     k_pool = np.zeros_like(wl.k_pool)
     j_star = 5
     slot = wl.block_tables[0, j_star // 16]
-    k_pool[slot, 0, j_star % 16, 0] = f32_to_bf16_bits(np.float32(1.0))
+    k_pool[slot, 0, j_star % 16, 0] = f32_to_bf16_bits(np.float32(1.0)).item()
     q = np.zeros_like(wl.q)
-    q_val = f32_to_bf16_bits(np.float32(50.0 / wl.scale))
+    q_val = f32_to_bf16_bits(np.float32(50.0 / wl.scale)).item()
     q[:, 0, 0] = q_val
     logit = float(oracle.bf16_bits_to_f64(np.array([q_val]))[0]) * wl.scale
     assert logit > 49
