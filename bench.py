@@ -208,6 +208,92 @@ def bench_copy(args, dev):
             "cpu_baseline": None}
 
 
+def bench_control_plane(args):
+    """The host-side control plane (cs_scout_*) on a synthetic agent trace:
+    24 agents whose successor is a fixed one 80% of the time, each turn
+    touching 64 blocks of a 16384-block pool.  Native costs come from batched
+    calls (no per-touch FFI); per-call costs include one ctypes round trip,
+    reported alongside as `ffi_floor_us`.  Host only: no GPU is used."""
+    import numpy as np
+    from paper_2608_14624_amd import ops
+    import oracle.control_plane as oracle_cp
+
+    agents, blocks, per_turn, turns = 24, 16384, 64, 4096
+    rng = np.random.default_rng(11)
+    succ = rng.permutation(agents)
+    seq = np.empty(turns, dtype=np.int32)
+    a = 0
+    for t in range(turns):
+        seq[t] = a
+        a = succ[a] if rng.random() < 0.8 else rng.integers(agents)
+    tr_agents = np.repeat(seq, per_turn)
+    tr_blocks = rng.integers(0, blocks, tr_agents.size, dtype=np.int32)
+    tr_tokens = np.full(tr_agents.size, 16, dtype=np.int32)
+    tr_now = np.repeat(np.arange(turns, dtype=np.int64), per_turn)
+    dispatches = int(np.count_nonzero(np.diff(seq)) + 1)
+
+    def best_of(fn, reps=5):
+        best = float("inf")
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            fn()
+            best = min(best, time.perf_counter() - t0)
+        return best
+
+    def replay():
+        sc = ops.Scout(agents, blocks)
+        sc.observe_touches(tr_blocks, tr_agents, tr_tokens, tr_now)
+        return sc
+    t_trace = best_of(replay)
+    # every touch a dispatch: the transition update plus the hop-table rebuild
+    alt = np.tile(np.arange(agents, dtype=np.int32), 2000)
+    alt_b = rng.integers(0, blocks, alt.size, dtype=np.int32)
+    alt_tok = np.full(alt.size, 16, dtype=np.int32)
+    alt_now = np.arange(alt.size, dtype=np.int64)
+    sc = replay()
+    t_disp = best_of(lambda: sc.observe_touches(alt_b, alt, alt_tok, alt_now))
+
+    n_calls = 20000
+    floor = best_of(lambda: [sc.current for _ in range(n_calls)]) / n_calls
+    t_surv = best_of(lambda: [sc.survival_all() for _ in range(n_calls // 10)]) / (n_calls // 10)
+    cands = [int(b) for b in rng.integers(0, blocks, 32)]
+    t_victim = best_of(lambda: [sc.select_victim(cands, turns) for _ in range(n_calls)]) / n_calls
+    t_between = best_of(lambda: [sc.between_step() for _ in range(n_calls)]) / n_calls
+
+    # the oracle on a bounded prefix of the same trace
+    n_or = 20000
+    t0 = time.perf_counter()
+    plane = oracle_cp.ControlPlane(agents, blocks)
+    for i in range(n_or):
+        plane.observe_touch(int(tr_blocks[i]), int(tr_agents[i]), 16, int(tr_now[i]))
+    t_oracle = time.perf_counter() - t0
+
+    touch_us = t_trace / tr_agents.size * 1e6
+    return {"metric": "control-plane ObserveTouch us per block touch (host)",
+            "value": round(touch_us, 4), "unit": "us", "n_gpus": 0, "steps": 1, "warmup": 0,
+            "ms_per_step": round(t_trace * 1e3, 3), "higher_is_better": False,
+            "scaling": "weak", "vs_baseline": round(touch_us / 1.0, 4), "dtype": "f64",
+            "data": "synthetic",
+            "config": {"workload": f"{agents} agents, {turns} turns x {per_turn} block touches, "
+                                   f"{blocks}-block pool, dominant successor p=0.8",
+                       "touches": int(tr_agents.size), "dispatches": dispatches},
+            "control_plane": {
+                "observe_touch_us": round(touch_us, 4),
+                "dispatch_us": round(t_disp / alt.size * 1e6, 4),
+                "survival_all_us": round(t_surv * 1e6, 3),
+                "select_victim_32_us": round(t_victim * 1e6, 3),
+                "between_step_us": round(t_between * 1e6, 3),
+                "ffi_floor_us": round(floor * 1e6, 3),
+                "state_bytes_24_agents": ops.Scout(agents, 0).state_bytes(),
+                "state_bytes_with_pool": sc.state_bytes(),
+                "paper": {"observe_touch_us": 1.0, "predict_survival_us": 6.0,
+                          "state_bytes": 25 * 1024}},
+            "roofline": None,
+            "cpu_baseline": {"value": round(t_oracle / n_or * 1e6, 3), "unit": "us", "cores": 1,
+                             "kind": "oracle",
+                             "sample": f"first {n_or} touches of the same trace"}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -217,10 +303,11 @@ def main():
                     choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--component", default="pipeline",
-                    choices=("pipeline", "kv_write", "kv_offload", "decode"),
+                    choices=("pipeline", "kv_write", "kv_offload", "decode", "control_plane"),
                     help="pipeline (default): the serving step; kv_write / kv_offload: "
                          "the write-back scatter and the offload copy on their own; "
-                         "decode: paged decode attention (use --workload decode_batch)")
+                         "decode: paged decode attention (use --workload decode_batch); "
+                         "control_plane: the host-side scout on a synthetic agent trace")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a plain 1 GiB device-to-device copy (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -230,6 +317,10 @@ def main():
               "shards by KV head or by invocation with no exchange inside it, see the "
               "design notes)", file=sys.stderr)
         sys.exit(2)
+
+    if args.component == "control_plane":
+        print(json.dumps(bench_control_plane(args)), flush=True)
+        return
 
     import numpy as np
     import torch
@@ -281,20 +372,8 @@ def main():
             dw.attention(stream=main_stream)
             a_ev[si][0][1].record(main_stream)
             return
-        # same order as AgentPipeline.step, with events around each launch
-        for k, a in enumerate(pipe.agents):
-            nxt = pipe.agents[(k + 1) % n_launch]
-            if k == 0:
-                pipe.side.wait_stream(main_stream)
-            with torch.cuda.stream(pipe.side):
-                p_ev[si][k][0].record(pipe.side)
-                pipe.prefetch_agent(nxt, pipe.side)
-                p_ev[si][k][1].record(pipe.side)
-                pipe.events[nxt].record(pipe.side)
-            a_ev[si][k][0].record(main_stream)
-            pipe.batches[k].attention(stream=main_stream)
-            a_ev[si][k][1].record(main_stream)
-            main_stream.wait_event(pipe.events[nxt])
+        # AgentPipeline.step with events around each launch
+        pipe.step(timing=list(zip(p_ev[si], a_ev[si])))
 
     torch.cuda.synchronize()
     t0 = time.perf_counter()

@@ -27,10 +27,11 @@
  *                            paged KV (the decode that follows a prefill).
  *
  * Conventions shared by all calls
- *   - Every pointer is caller-owned.  The library allocates no device or host
- *     memory and keeps no state beyond a per-process cache of device
- *     properties; calls are reentrant and may run concurrently on different
- *     streams.
+ *   - Every pointer is caller-owned.  The GPU calls allocate no device or
+ *     host memory and keep no state beyond a per-process cache of device
+ *     properties; they are reentrant and may run concurrently on different
+ *     streams.  The control plane (cs_scout_*, at the end of this file) is
+ *     host-only and owns the host memory behind its handle.
  *   - Every call enqueues its kernel on `stream` (NULL = the legacy default
  *     stream of the current device) and return without synchronizing.  Device
  *     metadata is read by the kernels, never by the host, so the calls can be
@@ -235,6 +236,123 @@ int cs_kv_offload(const int32_t *src_block_ids, int32_t n, const void *k_pool,
                   const void *v_pool, int32_t num_blocks, void *host_k_blocks,
                   void *host_v_blocks, int32_t num_kv_heads, int32_t head_dim,
                   int32_t block_size, cs_stream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Control plane (host only): the agent-transition learner, the survival
+ * scorer and the prefetch coordinator of Sec. 3.2-3.4, driven as in the
+ * runtime workflow algorithm of Sec. 3 (a block touch updates the block's
+ * metadata; a touch by another agent than the current one is a dispatch:
+ * the transition is counted, the thresholded graph and the hop table are
+ * rebuilt from the new agent, and it becomes current).
+ *
+ * Agents are dense ids in [0, num_agents) (cs_scout_agent_id maps a
+ * prompt-prefix fingerprint to one); blocks are pool slots in
+ * [0, num_blocks).  Times are caller-defined integer ticks (the paper uses
+ * scheduler steps); ages are `now - last access`.
+ *
+ * A handle is not thread-safe: calls on one handle must not overlap.
+ * Handles are independent of each other and of the GPU calls.  Functions
+ * that return a status fail with CS_ERR_INVALID_ARG (message in
+ * cs_last_error()); queries with an out-of-range argument return -1 (ids)
+ * or NaN (probabilities, scores).  A NULL handle is CS_ERR_INVALID_ARG,
+ * -1 or NaN likewise.
+ * ------------------------------------------------------------------------ */
+
+typedef struct cs_scout cs_scout;
+
+/* Hyperparameters.  The paper names them without values; the defaults are
+ * this library's reading. */
+typedef struct cs_scout_params {
+    double eps;     /* Eq. (3) additive smoothing, > 0            (0.1)  */
+    double tau;     /* Eq. (7) edge confidence threshold, [0, 1]  (0.2)  */
+    int32_t e_max;  /* Eq. (8) hop horizon E_max, > 0             (4)    */
+    double lambda;  /* Eq. (9) recency decay per tick, >= 0       (0.1)  */
+    double delta;   /* Eq. (9) floor of both factors, >= 0        (0.05) */
+    double r_min;   /* Eq. (11) predictability gate, finite       (0.3)  */
+} cs_scout_params;
+
+/* Fill *out with the defaults above. */
+void cs_scout_default_params(cs_scout_params *out);
+
+/* Create a control plane for up to num_agents agents (1..4096) and
+ * num_blocks pool slots (>= 0).  params NULL = defaults.  On success *out
+ * owns O(num_agents^2 + num_blocks) host memory (cs_scout_state_bytes);
+ * release it with cs_scout_destroy.  On failure *out is NULL. */
+int cs_scout_create(int32_t num_agents, int32_t num_blocks,
+                    const cs_scout_params *params, cs_scout **out);
+
+/* Release a handle (NULL is a no-op). */
+void cs_scout_destroy(cs_scout *s);
+
+/* Dense agent id of a prompt-prefix fingerprint (the agent anchor's hash,
+ * Sec. 3.1): a known fingerprint returns its id, a new one the next free
+ * id in arrival order, or -1 once num_agents ids are taken. */
+int32_t cs_scout_agent_id(cs_scout *s, uint64_t fingerprint);
+
+/* Record that `agent` touched pool slot `block` holding `tokens` tokens
+ * (>= 0) at time `now`.  If `agent` differs from the current agent this is
+ * a dispatch: C[current][agent] += 1 (when there is a current agent), the
+ * hop table is rebuilt by breadth-first search from `agent` over the edges
+ * of Eq. (7), and `agent` becomes current.  O(1) without a dispatch,
+ * O(num_agents^2) with one. */
+int cs_scout_observe_touch(cs_scout *s, int32_t block, int32_t agent,
+                           int32_t tokens, int64_t now);
+
+/* cs_scout_observe_touch for touches i = 0..n-1 in order (host arrays of n
+ * entries): the block pool's prefix match of one request touches all its
+ * prefix blocks at once.  Every entry is validated before any is applied;
+ * on an error nothing changes. */
+int cs_scout_observe_touches(cs_scout *s, const int32_t *blocks, const int32_t *agents,
+                             const int32_t *tokens, const int64_t *now, int32_t n);
+
+/* The current agent, -1 before the first touch. */
+int32_t cs_scout_current(const cs_scout *s);
+
+/* Eq. (3): P(j | i) = (C_ij + eps) / (sum_k C_ik + num_agents * eps). */
+double cs_scout_transition_prob(const cs_scout *s, int32_t i, int32_t j);
+
+/* Eq. (5): argmax_j P(j | current), lowest id on ties; -1 before the first
+ * touch. */
+int32_t cs_scout_predict(const cs_scout *s);
+
+/* Eq. (8): 1 - min(E[a], e_max) / e_max with E[a] the hop distance from the
+ * current agent in the graph of Eq. (7); 0 if unreachable or before the
+ * first touch. */
+double cs_scout_survival(const cs_scout *s, int32_t agent);
+
+/* Eq. (8) for every agent into out[0..num_agents) (host array): the table
+ * the paper computes once per scheduler step (Sec. 4). */
+int cs_scout_survival_all(const cs_scout *s, double *out);
+
+/* Eq. (9): (survival(owner) + delta) * (exp(-lambda * (now - last access))
+ * + delta) * tokens, for the block's last toucher (survival 0 for a block
+ * never touched, whose tokens are 0 as well). */
+double cs_scout_score_block(const cs_scout *s, int32_t block, int64_t now);
+
+/* Mark whether a block's contents are also resident in the CPU tier (e.g.
+ * after cs_kv_offload); eviction prefers such blocks among equal scores
+ * (Sec. 4).  resident: 0 or non-zero. */
+int cs_scout_set_host_resident(cs_scout *s, int32_t block, int32_t resident);
+
+/* The eviction victim among candidates[0..n) (host array): the block with
+ * the lowest score; among equal scores a CPU-resident one; then the first.
+ * -1 if n <= 0, candidates is NULL or any candidate is out of range. */
+int32_t cs_scout_select_victim(const cs_scout *s, const int32_t *candidates,
+                               int32_t n, int64_t now);
+
+/* Eq. (2) over the observed transitions: 1 - H(next | current) / H(next)
+ * of their empirical joint distribution; 0 with no transition, 1 when
+ * every transition has the same successor. */
+double cs_scout_predictability(const cs_scout *s);
+
+/* Eq. (10)-(11), the between-step decision: the agent whose anchor to
+ * prefetch (cs_scout_predict) when predictability >= r_min, else -1. */
+int32_t cs_scout_between_step(const cs_scout *s);
+
+/* Host bytes of the decision state: transition counts, row and column
+ * totals, row entropies, hop table and the per-block tables (excludes the
+ * fingerprint map): 4 A^2 + 28 A + 17 num_blocks for A = num_agents. */
+int64_t cs_scout_state_bytes(const cs_scout *s);
 
 /* Static, NUL-terminated name of a status code ("CS_OK", ...). */
 const char *cs_status_string(int status);

@@ -2,7 +2,8 @@
 
     python -m paper_2608_14624_amd.build
 
-compiles every ``csrc/*.hip`` source into ``paper_2608_14624_amd/libcachescout.so``.
+compiles every ``csrc/*.hip`` source (and the host-only ``csrc/*.cpp``) into
+``paper_2608_14624_amd/libcachescout.so``.
 """
 
 import glob
@@ -10,6 +11,7 @@ import os
 import shutil
 import subprocess
 import sys
+import tempfile
 
 PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG_DIR)
@@ -25,25 +27,48 @@ def hipcc():
     return path
 
 
-def build(verbose=False):
-    """Compile the HIP sources into the shared library and return its path."""
-    sources = sorted(glob.glob(os.path.join(PKG_DIR, "csrc", "*.hip")))
-    tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-           # keep the compiler from forming packed fp32 ops
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           # MFMA accumulators in arch VGPRs: the softmax rescale then works on
-           # them in place instead of copying them out of AGPRs every step
-           "-mllvm", "-amdgpu-mfma-vgpr-form",
-           "-Wall", "-Wno-unused-result",
-           "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG_DIR, "csrc"),
-           *sources, "-o", tmp]
+def cxx():
+    path = shutil.which("g++") or shutil.which("c++")
+    if not path:
+        raise RuntimeError("no host C++ compiler (g++) found")
+    return path
+
+
+def run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {res.returncode}")
+        raise RuntimeError(f"{os.path.basename(cmd[0])} failed with exit code {res.returncode}")
+
+
+def build(verbose=False):
+    """Compile the HIP sources and the host-only C++ into the shared library
+    and return its path."""
+    sources = sorted(glob.glob(os.path.join(PKG_DIR, "csrc", "*.hip")))
+    host_sources = sorted(glob.glob(os.path.join(PKG_DIR, "csrc", "*.cpp")))
+    includes = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG_DIR, "csrc")]
+    tmp = LIB_PATH + ".tmp"
+    with tempfile.TemporaryDirectory(prefix="cachescout_build_") as work:
+        # the control plane: plain host C++ built by the host compiler, with no
+        # fused multiply-adds so its fp64 threshold decisions are the
+        # expressions as written
+        objects = []
+        for src in host_sources:
+            obj = os.path.join(work, os.path.basename(src) + ".o")
+            run([cxx(), "-O2", "-std=c++17", "-fPIC", "-ffp-contract=off",
+                 "-Wall", "-Wextra", *includes, "-c", src, "-o", obj], verbose)
+            objects.append(obj)
+        run([hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+             # keep the compiler from forming packed fp32 ops
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             # MFMA accumulators in arch VGPRs: the softmax rescale then works on
+             # them in place instead of copying them out of AGPRs every step
+             "-mllvm", "-amdgpu-mfma-vgpr-form",
+             "-Wall", "-Wno-unused-result", *includes,
+             # hipcc compiles every input as HIP unless told otherwise
+             *sources, "-x", "none", *objects, "-o", tmp], verbose)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
 

@@ -2,6 +2,7 @@
 // optional metadata checks (CS_DEBUG_CHECK=1) and kernel launches.  The
 // operations themselves are described in include/cachescout.h.
 #include "cachescout.h"
+#include "error.h"
 #include "internal.h"
 
 #include <math.h>
@@ -13,8 +14,10 @@
 #include <vector>
 
 namespace {
-
 thread_local char g_last_error[512];
+}  // namespace
+
+namespace cs {
 
 int fail(int status, const char* fmt, ...) {
   va_list ap;
@@ -28,6 +31,13 @@ int ok() {
   g_last_error[0] = '\0';
   return CS_OK;
 }
+
+}  // namespace cs
+
+namespace {
+
+using cs::fail;
+using cs::ok;
 
 int hip_fail(hipError_t e, const char* what) {
   return fail(CS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));

@@ -21,7 +21,20 @@ CS_ERR_HIP = 3
 
 # every symbol the C header declares
 EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_kv_write", "cs_kv_offload",
-            "cs_paged_decode_attn", "cs_status_string", "cs_last_error")
+            "cs_paged_decode_attn", "cs_status_string", "cs_last_error",
+            "cs_scout_default_params", "cs_scout_create", "cs_scout_destroy",
+            "cs_scout_agent_id", "cs_scout_observe_touch", "cs_scout_current",
+            "cs_scout_transition_prob", "cs_scout_predict", "cs_scout_survival",
+            "cs_scout_score_block", "cs_scout_select_victim", "cs_scout_predictability",
+            "cs_scout_between_step", "cs_scout_state_bytes", "cs_scout_set_host_resident",
+            "cs_scout_survival_all", "cs_scout_observe_touches")
+
+
+class ScoutParams(ctypes.Structure):
+    """``cs_scout_params``: the control plane's hyperparameters."""
+    _fields_ = [("eps", ctypes.c_double), ("tau", ctypes.c_double), ("e_max", ctypes.c_int32),
+                ("lam", ctypes.c_double), ("delta", ctypes.c_double),
+                ("r_min", ctypes.c_double)]
 
 
 class CacheScoutError(RuntimeError):
@@ -53,6 +66,31 @@ def _load():
     lib.cs_status_string.restype = ctypes.c_char_p
     lib.cs_last_error.argtypes = []
     lib.cs_last_error.restype = ctypes.c_char_p
+    i64, u64, f64, h = ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_void_p
+    sigs = {
+        "cs_scout_default_params": ([ctypes.POINTER(ScoutParams)], None),
+        "cs_scout_create": ([i32, i32, ctypes.POINTER(ScoutParams), ctypes.POINTER(h)],
+                            ctypes.c_int),
+        "cs_scout_destroy": ([h], None),
+        "cs_scout_agent_id": ([h, u64], i32),
+        "cs_scout_observe_touch": ([h, i32, i32, i32, i64], ctypes.c_int),
+        "cs_scout_current": ([h], i32),
+        "cs_scout_transition_prob": ([h, i32, i32], f64),
+        "cs_scout_predict": ([h], i32),
+        "cs_scout_survival": ([h, i32], f64),
+        "cs_scout_score_block": ([h, i32, i64], f64),
+        "cs_scout_select_victim": ([h, ctypes.POINTER(i32), i32, i64], i32),
+        "cs_scout_predictability": ([h], f64),
+        "cs_scout_between_step": ([h], i32),
+        "cs_scout_state_bytes": ([h], i64),
+        "cs_scout_set_host_resident": ([h, i32, i32], ctypes.c_int),
+        "cs_scout_survival_all": ([h, ctypes.POINTER(f64)], ctypes.c_int),
+        "cs_scout_observe_touches": ([h, vp, vp, vp, vp, i32], ctypes.c_int),
+    }
+    for name, (args, res) in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
     return lib
 
 
@@ -268,3 +306,104 @@ def cs_paged_decode_attn(q, k_pool, v_pool, block_tables, seq_lens, out, *, max_
                                     _ptr(seq_lens), batch, int(max_seq_len), block_tables.shape[1],
                                     num_blocks, hq, hkv, d, bs, float(scale), _ptr(out),
                                     _stream_handle(stream, dev)))
+
+
+def scout_default_params():
+    p = ScoutParams()
+    _lib.cs_scout_default_params(ctypes.byref(p))
+    return p
+
+
+class Scout:
+    """Owner of a ``cs_scout`` handle: the host-side control plane (transition
+    learner, survival scorer, prefetch coordinator).  Methods map one to one
+    onto the ``cs_scout_*`` calls; -1 from the C side becomes ``None``."""
+
+    def __init__(self, num_agents, num_blocks, **params):
+        prm = scout_default_params()
+        for k, v in params.items():
+            if not hasattr(prm, k):
+                raise TypeError(f"unknown control-plane parameter {k!r}")
+            setattr(prm, k, v)
+        handle = ctypes.c_void_p()
+        _check(_lib.cs_scout_create(int(num_agents), int(num_blocks), ctypes.byref(prm),
+                                    ctypes.byref(handle)))
+        self._h = handle
+        self._destroy = _lib.cs_scout_destroy   # still reachable at interpreter exit
+        self.num_agents = int(num_agents)
+        self.num_blocks = int(num_blocks)
+        self.params = prm
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.close()
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    @staticmethod
+    def _opt(v):
+        return None if v < 0 else v
+
+    def agent_id(self, fingerprint):
+        return self._opt(_lib.cs_scout_agent_id(self._h, fingerprint & 0xFFFFFFFFFFFFFFFF))
+
+    def observe_touch(self, block, agent, tokens, now):
+        _check(_lib.cs_scout_observe_touch(self._h, block, agent, tokens, now))
+
+    def observe_touches(self, blocks, agents, tokens, now):
+        """Batched touches from four equal-length int32/int32/int32/int64
+        numpy arrays (C-contiguous)."""
+        import numpy as np
+        arrs = [np.ascontiguousarray(blocks, dtype=np.int32),
+                np.ascontiguousarray(agents, dtype=np.int32),
+                np.ascontiguousarray(tokens, dtype=np.int32),
+                np.ascontiguousarray(now, dtype=np.int64)]
+        n = len(arrs[0])
+        if any(len(a) != n for a in arrs):
+            raise CacheScoutError(CS_ERR_INVALID_ARG, "touch arrays differ in length")
+        _check(_lib.cs_scout_observe_touches(self._h, *(a.ctypes.data for a in arrs), n))
+
+    @property
+    def current(self):
+        return self._opt(_lib.cs_scout_current(self._h))
+
+    def transition_prob(self, i, j):
+        return _lib.cs_scout_transition_prob(self._h, i, j)
+
+    def predict(self):
+        return self._opt(_lib.cs_scout_predict(self._h))
+
+    def survival(self, agent):
+        return _lib.cs_scout_survival(self._h, agent)
+
+    def score_block(self, block, now):
+        return _lib.cs_scout_score_block(self._h, block, now)
+
+    def set_host_resident(self, block, resident):
+        _check(_lib.cs_scout_set_host_resident(self._h, block, 1 if resident else 0))
+
+    def survival_all(self):
+        out = (ctypes.c_double * self.num_agents)()
+        _check(_lib.cs_scout_survival_all(self._h, out))
+        return list(out)
+
+    def select_victim(self, candidates, now):
+        arr = (ctypes.c_int32 * len(candidates))(*candidates)
+        return self._opt(_lib.cs_scout_select_victim(self._h, arr, len(candidates), now))
+
+    def predictability(self):
+        return _lib.cs_scout_predictability(self._h)
+
+    def between_step(self):
+        return self._opt(_lib.cs_scout_between_step(self._h))
+
+    def state_bytes(self):
+        return _lib.cs_scout_state_bytes(self._h)

@@ -7,14 +7,21 @@ background prefetch (arXiv 2608.14624, Sec. 3.4: while the current agent is
 served, the anchor of the predicted next agent, Eq. (10), is brought in off
 the critical path): for each agent in dispatch order,
 
-    side stream : cs_kv_prefetch(next agent's CPU-tier blocks); record event
+    side stream : wait until the target's last attention has finished,
+                  cs_kv_prefetch(target agent's CPU-tier blocks), record event
     main stream : cs_prefill_paged_attn(this agent's invocations)
     main stream : wait for the event before the next agent's attention
 
-The destination slots of a prefetch belong to the next agent only, so the
-attention in flight never reads them (no hazard by construction).  Only the
-two C calls do work; this module orders them.
+The target is the next agent in dispatch order (the known-order protocol),
+or, with a :class:`ScoutPolicy`, the control plane's between-step decision
+(Eq. (10)-(11)); a wrong or withheld prediction is a miss, and the next
+agent's blocks are then brought in on the main stream, on the critical path.
+A prefetch rewrites only its target's slots, after the target's last reader
+has finished, so the attention in flight never sees a slot being written.
+Only the C calls do work; this module orders them.
 """
+
+import hashlib
 
 import numpy as np
 import torch
@@ -103,14 +110,64 @@ class DeviceWorkload:
         return self.out.view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-class AgentPipeline:
-    """Per-agent attention with the next agent's prefetch overlapped on a side stream.
+def agent_fingerprint(block_ids):
+    """64-bit fingerprint of an agent from its anchor's leading block ids (the
+    block pool's prefix hashes play this role in a serving engine, Sec. 4)."""
+    digest = hashlib.blake2b(np.ascontiguousarray(block_ids, dtype=np.int32).tobytes(),
+                             digest_size=8).digest()
+    return int.from_bytes(digest, "little")
 
-    Requires the invocations to be packed grouped by agent (each agent's
-    invocations contiguous), as the dispatch-ordered configurations are.
+
+class ScoutPolicy:
+    """Prefetch targets from the control plane (cs_scout_*).
+
+    Every turn reports the agent's prefix-block touches (the block pool's
+    prefix match, one call per turn) and then asks the between-step decision
+    for the agent to warm up next.  Host-only; usable without a GPU.
     """
 
-    def __init__(self, dw, side_stream=None):
+    def __init__(self, wl, agents, **params):
+        self.scout = ops.Scout(max(len(agents), 1), wl.num_blocks, **params)
+        self.ids, self.by_id, self.touches = {}, {}, {}
+        for a in agents:
+            invs = [r for r, inv in enumerate(wl.invocations) if inv.agent == a]
+            blocks, tokens = [], []
+            for r in invs:
+                p = int(wl.prefix_lens[r])
+                nb = -(-p // 16)
+                blocks.append(wl.block_tables[r, :nb])
+                tokens.append(np.minimum(16, p - 16 * np.arange(nb)))
+            blocks = np.concatenate(blocks) if blocks else np.zeros(0, np.int32)
+            tokens = np.concatenate(tokens) if tokens else np.zeros(0, np.int32)
+            blocks, first = np.unique(blocks, return_index=True)
+            lead = wl.block_tables[invs[0], :4] if invs else np.zeros(0, np.int32)
+            aid = self.scout.agent_id(agent_fingerprint(lead))
+            if aid in self.by_id:
+                raise ValueError(f"agents {self.by_id[aid]} and {a} share a fingerprint")
+            self.ids[a], self.by_id[aid] = aid, a
+            self.touches[a] = (blocks.astype(np.int32), tokens[first].astype(np.int32))
+        self.now = 0
+
+    def on_turn(self, a):
+        """Record agent ``a``'s turn; return the agent to prefetch, or None."""
+        blocks, tokens = self.touches[a]
+        n = len(blocks)     # an agent with no cached prefix touches nothing
+        self.scout.observe_touches(blocks, np.full(n, self.ids[a], np.int32), tokens,
+                                   np.full(n, self.now, np.int64))
+        self.now += 1
+        t = self.scout.between_step()
+        return None if t is None else self.by_id.get(t)
+
+
+class AgentPipeline:
+    """Per-agent attention with a prefetch overlapped on a side stream.
+
+    Requires the invocations to be packed grouped by agent (each agent's
+    invocations contiguous) and at least two agents.  ``policy``: None for the
+    known dispatch order, or a :class:`ScoutPolicy`.
+    """
+
+    def __init__(self, dw, side_stream=None, policy=None):
         wl = dw.wl
         agents = [inv.agent for inv in wl.invocations]
         order = []
@@ -119,8 +176,11 @@ class AgentPipeline:
                 order.append(a)
         if len(order) != len(set(order)):
             raise ValueError("invocations must be grouped by agent")
+        if len(order) < 2:
+            raise ValueError("the pipeline needs at least two agents")
         self.dw = dw
         self.agents = order
+        self.policy = policy
         self.batches = []
         lo = 0
         for a in order:
@@ -141,10 +201,12 @@ class AgentPipeline:
                 assert i1 - i0 == len(idx), "prefetch blocks must be grouped by agent"
                 self.prefetch[a] = (dw.host_k[i0:i1], dw.host_v[i0:i1], dw.prefetch_dst[i0:i1])
         self.side = side_stream if side_stream is not None else torch.cuda.Stream(dw.device)
-        self.events = {a: torch.cuda.Event() for a in order}
+        self.events = {a: torch.cuda.Event() for a in order}       # prefetch done
+        self.attn_done = {a: torch.cuda.Event() for a in order}    # last reader done
         self.flops = sum(b.flops for b in self.batches)
         self.prefetch_bytes = sum(int(k.numel() * 2 + v.numel() * 2)
                                   for k, v, _ in self.prefetch.values())
+        self.hits = self.misses = 0
 
     def prefetch_agent(self, a, stream):
         if a in self.prefetch:
@@ -156,22 +218,41 @@ class AgentPipeline:
         main = torch.cuda.current_stream(self.dw.device)
         self.prefetch_agent(self.agents[0], main)
 
-    def step(self):
-        """One pass over all agents; the next agent's prefetch overlaps this agent's attention.
+    def step(self, timing=None):
+        """One pass over all agents; each turn's prefetch overlaps its attention.
 
-        The last agent's turn prefetches the first agent again (for the next
-        pass), so every pass moves every agent's CPU-tier blocks once.
+        With the known order the last turn prefetches the first agent again
+        (for the next pass), so every pass moves every agent's CPU-tier blocks
+        once.  ``timing``: optional per-turn ``((p0, p1), (a0, a1))`` timing
+        events recorded around the side-stream prefetch and the attention.
         """
         main = torch.cuda.current_stream(self.dw.device)
         n = len(self.agents)
         for k, a in enumerate(self.agents):
             nxt = self.agents[(k + 1) % n]
-            if k == 0:
-                # slots rewritten in this pass were last read by attention
-                # already enqueued on the main stream
-                self.side.wait_stream(main)
-            with torch.cuda.stream(self.side):
-                self.prefetch_agent(nxt, self.side)
-                self.events[nxt].record(self.side)
+            target = nxt if self.policy is None else self.policy.on_turn(a)
+            (p0, p1), (a0, a1) = timing[k] if timing is not None else ((None, None),) * 2
+            if target is not None and target != a:
+                self.side.wait_event(self.attn_done[target])
+                with torch.cuda.stream(self.side):
+                    if p0 is not None:
+                        p0.record(self.side)
+                    self.prefetch_agent(target, self.side)
+                    if p1 is not None:
+                        p1.record(self.side)
+                    self.events[target].record(self.side)
+            if a0 is not None:
+                a0.record(main)
             self.batches[k].attention(stream=main)
-            main.wait_event(self.events[nxt])
+            if a1 is not None:
+                a1.record(main)
+            self.attn_done[a].record(main)
+            if target == nxt:
+                self.hits += 1
+                main.wait_event(self.events[nxt])
+            else:
+                # a miss: the next agent's blocks come in on the critical path
+                # (after any side-stream write still in flight)
+                self.misses += 1
+                main.wait_stream(self.side)
+                self.prefetch_agent(nxt, main)

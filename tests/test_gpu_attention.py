@@ -123,6 +123,34 @@ def test_llama70b_prefetch_pipeline_sampled(P):
     assert torch.isfinite(dw.out.float()).all().item()
 
 
+def test_llama70b_prefetch_pipeline_driven_by_the_control_plane(P):
+    """The same workload with the prefetch target chosen by the control plane
+    (cs_scout_*): three passes, misses only while it learns the cycle, and
+    the same outputs and pools as the oracle."""
+    _, pipeline = P
+    wl = make_config("llama70b_prefetch")
+    print(f"[case] llama70b_prefetch scout-driven pipeline total_q={wl.total_q}", flush=True)
+    dw = pipeline.DeviceWorkload(wl)
+    agents = sorted({inv.agent for inv in wl.invocations})
+    pipe = pipeline.AgentPipeline(dw, policy=pipeline.ScoutPolicy(wl, agents))
+    pipe.stage_first()
+    for p in range(3):
+        dw.out.fill_(float("nan"))
+        pipe.step()
+        torch.cuda.synchronize()
+        print(f"    pass {p}: hits={pipe.hits} misses={pipe.misses}", flush=True)
+    n = len(pipe.agents)
+    assert pipe.misses == n - 1 and pipe.hits == 2 * n + 1
+    kp, vp = oracle.kv_prefetch(wl.host_k, wl.host_v, wl.prefetch_dst, wl.k_pool, wl.v_pool)
+    samples = sample_rows(wl, 300, seed=4)
+    mx, mean = compare_rows(wl, dw.out_bits(), samples, kp, vp)
+    print(f"    {len(samples)} rows: max_abs={mx:.3e} mean_abs={mean:.3e}", flush=True)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+    assert np.array_equal(dw.k_pool.view(torch.int16).cpu().numpy().view(np.uint16), kp)
+    assert np.array_equal(dw.v_pool.view(torch.int16).cpu().numpy().view(np.uint16), vp)
+    assert torch.isfinite(dw.out.float()).all().item()
+
+
 @pytest.mark.slow
 def test_long_mixed_sampled(P):
     _, pipeline = P
