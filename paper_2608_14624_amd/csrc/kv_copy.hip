@@ -10,15 +10,14 @@
 //
 // Offload (Sec. 4: blocks leaving the GPU are kept in the CPU tier): whole
 // blocks are copied from pool slots to pinned host memory, the reverse of
-// the prefetch.  One work-group moves one block's K or V (32 KiB at 8 x 16 x
-// 128) with 16-byte loads from HBM and 16-byte stores that go over the host
-// link through the buffer's device mapping.
+// the prefetch, by the same few persistent work-groups (block_copy.h): 16-byte
+// loads from HBM and non-temporal 16-byte stores that go over the host link
+// through the buffer's device mapping.
+#include "block_copy.h"
 #include "internal.h"
 
 namespace cs {
 namespace {
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
 constexpr int kTokensPerWG = kThreads / 64;
@@ -48,30 +47,14 @@ __global__ __launch_bounds__(kThreads) void kv_write_kernel(
   }
 }
 
-constexpr int kUnroll = 8;
-
-__global__ __launch_bounds__(kThreads) void kv_offload_kernel(
+__global__ __launch_bounds__(kCopyThreads) void kv_offload_kernel(
     const int32_t* __restrict__ src_ids, const u32x4* __restrict__ k_pool,
     const u32x4* __restrict__ v_pool, u32x4* __restrict__ host_k, u32x4* __restrict__ host_v,
-    long long vecs_per_block) {
-  const int i = blockIdx.x >> 1;
-  const bool is_v = blockIdx.x & 1;
-  const size_t slot = (size_t)src_ids[i];
-  const u32x4* src = (is_v ? v_pool : k_pool) + slot * vecs_per_block;
-  u32x4* dst = (is_v ? host_v : host_k) + (size_t)i * vecs_per_block;
-  for (long long base = 0; base < vecs_per_block; base += (long long)kThreads * kUnroll) {
-    u32x4 v[kUnroll];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const long long idx = base + (long long)u * kThreads + threadIdx.x;
-      if (idx < vecs_per_block) v[u] = src[idx];
-    }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const long long idx = base + (long long)u * kThreads + threadIdx.x;
-      if (idx < vecs_per_block) __builtin_nontemporal_store(v[u], dst + idx);
-    }
-  }
+    int units, long long vecs_per_block) {
+  copy_units<false, true>(
+      units, vecs_per_block,
+      [=](int u) { return ((u & 1) ? v_pool : k_pool) + (size_t)src_ids[u >> 1] * vecs_per_block; },
+      [=](int u) { return ((u & 1) ? host_v : host_k) + (size_t)(u >> 1) * vecs_per_block; });
 }
 
 }  // namespace
@@ -87,11 +70,11 @@ hipError_t launch_kv_write(const KvWriteLaunch& a, hipStream_t stream) {
 }
 
 hipError_t launch_kv_offload(const KvOffloadLaunch& a, hipStream_t stream) {
-  const dim3 grid((unsigned)(2LL * a.n)), block(kThreads);
-  hipLaunchKernelGGL(kv_offload_kernel, grid, block, 0, stream, a.src_ids,
-                     reinterpret_cast<const u32x4*>(a.k_pool), reinterpret_cast<const u32x4*>(a.v_pool),
-                     reinterpret_cast<u32x4*>(a.host_k), reinterpret_cast<u32x4*>(a.host_v),
-                     a.block_bytes / 16);
+  const int units = 2 * a.n;
+  hipLaunchKernelGGL(kv_offload_kernel, dim3(copy_grid(units)), dim3(kCopyThreads), 0, stream,
+                     a.src_ids, reinterpret_cast<const u32x4*>(a.k_pool),
+                     reinterpret_cast<const u32x4*>(a.v_pool), reinterpret_cast<u32x4*>(a.host_k),
+                     reinterpret_cast<u32x4*>(a.host_v), units, a.block_bytes / 16);
   return hipGetLastError();
 }
 
