@@ -61,17 +61,16 @@ def source_hash(paths):
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload, kernel_hash):
-    """HBM traffic per attention launch from a committed rocprofv3 --pmc summary.
-
-    Only used while the kernel source is the one the counters were taken on.
-    """
+def load_traffic(kernel, workload, kernel_hash):
+    """HBM bytes per launch of `kernel` on `workload` from a committed
+    rocprofv3 --pmc summary (FETCH_SIZE + WRITE_SIZE, each scaled by a plain
+    copy's reading); None unless the kernel source is the one measured."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         data = json.load(f)
-    entry = data.get(workload)
+    entry = data.get(f"{kernel}|{workload}")
     if not entry or entry.get("kernel_sha") != kernel_hash:
         return None
     return entry.get("bytes_per_launch")
@@ -138,26 +137,49 @@ def bench_copy(args, dev):
     k_pool = torch.from_numpy(wl.k_pool.view(np.int16)).view(torch.bfloat16).to(dev)
     v_pool = torch.from_numpy(wl.v_pool.view(np.int16)).view(torch.bfloat16).to(dev)
     hkv, d = wl.num_kv_heads, wl.head_dim
-    if args.component == "decode":
-        from paper_2608_14624_amd.workload import decode_view
+    if args.component in ("decode", "cascade_decode"):
+        from paper_2608_14624_amd.workload import cascade_view, decode_view
+        # the batch ordered by agent group (the order cascade decode needs;
+        # plain decode runs on the same order)
+        cv = cascade_view(wl)
         q_np, seq_lens_np = decode_view(wl)
+        order = cv["order"]
+        q_np, seq_lens_np = np.ascontiguousarray(q_np[order]), np.ascontiguousarray(seq_lens_np[order])
+        bt_np = np.ascontiguousarray(wl.block_tables[order])
         q = torch.from_numpy(q_np.view(np.int16)).view(torch.bfloat16).to(dev)
         out = torch.empty_like(q)
-        bt = torch.from_numpy(wl.block_tables).to(dev)
+        bt = torch.from_numpy(bt_np).to(dev)
         seq_lens = torch.from_numpy(seq_lens_np).to(dev)
         max_len = int(seq_lens_np.max())
-        # bytes each sequence's attention reads (K and V of all its keys), plus q and out
-        moved = int(seq_lens_np.astype(np.int64).sum()) * hkv * d * 2 * 2 + 2 * q.numel() * 2
+        # K and V of every key every sequence attends to (what a per-sequence
+        # kernel reads), and the distinct pool blocks among them (the least a
+        # kernel must read from HBM); both plus q and out
+        qo = 2 * q.numel() * 2
+        logical = int(seq_lens_np.astype(np.int64).sum()) * hkv * d * 2 * 2 + qo
         unique_blocks = len(np.unique(np.concatenate(
-            [wl.block_tables[r, :-(-int(L) // 16)] for r, L in enumerate(seq_lens_np)])))
-        unique_bytes = unique_blocks * hkv * 16 * d * 2 * 2
+            [bt_np[r, :-(-int(L) // 16)] for r, L in enumerate(seq_lens_np)])))
+        unique_bytes = unique_blocks * hkv * 16 * d * 2 * 2 + qo
+        moved = unique_bytes
+        if args.component == "decode":
+            def fn():
+                ops.cs_paged_decode_attn(q, k_pool, v_pool, bt, seq_lens, out,
+                                         max_seq_len=max_len, scale=wl.scale, stream=stream)
+        else:
+            cu = torch.from_numpy(cv["cu_groups"]).to(dev)
+            shared = torch.from_numpy(cv["shared_lens"]).to(dev)
+            need = ops.cs_cascade_decode_workspace_bytes(wl.batch, wl.num_q_heads, d,
+                                                         cv["max_shared_len"])
+            ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
 
-        def fn():
-            ops.cs_paged_decode_attn(q, k_pool, v_pool, bt, seq_lens, out, max_seq_len=max_len,
-                                     scale=wl.scale, stream=stream)
+            def fn():
+                ops.cs_cascade_decode_attn(q, k_pool, v_pool, bt, seq_lens, cu, shared, out,
+                                           max_seq_len=max_len,
+                                           max_group_seqs=cv["max_group_seqs"],
+                                           max_shared_len=cv["max_shared_len"], scale=wl.scale,
+                                           workspace=ws, stream=stream)
         peak, bound = PEAK_HBM_GBS, "hbm"
-        unit_desc = (f"{wl.batch} sequences, {int(seq_lens_np.sum())} keys, "
-                     f"{unique_blocks} distinct pool blocks "
+        unit_desc = (f"{wl.batch} sequences in {len(cv['shared_lens'])} agent groups, "
+                     f"{int(seq_lens_np.sum())} keys, {unique_blocks} distinct pool blocks "
                      f"({unique_blocks * hkv * 16 * d * 4 / 1e6:.0f} MB of unique K/V)")
     elif args.component == "kv_write":
         # the suffix tokens of every invocation, written to their own slots
@@ -186,16 +208,24 @@ def bench_copy(args, dev):
         def fn():
             ops.cs_kv_offload(ids, k_pool, v_pool, host_k, host_v, stream=stream)
         peak, bound, unit_desc = PEAK_PCIE5_X16_GBS, "host_link", f"{n} blocks"
+    kernel, sources = {
+        "decode": ("paged_decode_attn_kernel", ("paper_2608_14624_amd/csrc/paged_decode_attn.hip",)),
+        "cascade_decode": ("prefill_paged_attn_kernel<128, true> + paged_decode_attn_kernel<128, true>",
+                           ("paper_2608_14624_amd/csrc/prefill_paged_attn.hip",
+                            "paper_2608_14624_amd/csrc/paged_decode_attn.hip")),
+        "kv_write": ("kv_write_kernel", ("paper_2608_14624_amd/csrc/kv_copy.hip",)),
+        "kv_offload": ("kv_offload_kernel", ("paper_2608_14624_amd/csrc/kv_copy.hip",
+                                             "paper_2608_14624_amd/csrc/block_copy.h")),
+    }[args.component]
+    traffic = load_traffic(kernel, args.workload, source_hash(sources))
     wall, avg_ms = _time_launches(fn, args.steps, args.warmup, stream)
     gbs = moved / (avg_ms * 1e-3) / 1e9
     extra = {}
-    if args.component == "decode":
-        # sequences of one agent share its anchor blocks, so most of the K/V
-        # a sequence reads was just read by another and comes from L2 / MALL
-        extra = {"unique_bytes": unique_bytes,
-                 "unique_rate_gbs": round(unique_bytes / (avg_ms * 1e-3) / 1e9, 2),
-                 "note": "achieved counts the K/V every sequence reads; shared anchor "
-                         "blocks are served from cache, so it can exceed the HBM peak"}
+    if args.component in ("decode", "cascade_decode"):
+        extra = {"logical_bytes": logical,
+                 "logical_rate_gbs": round(logical / (avg_ms * 1e-3) / 1e9, 2),
+                 "note": "achieved counts each distinct K/V block once (plus q and out); "
+                         "logical counts the K/V of every key of every sequence"}
     return {"metric": f"{args.component} GB/s, 1 MI355X", "value": round(gbs, 2), "unit": "GB/s",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
             "ms_per_step": round(wall / args.steps * 1e3, 4), "higher_is_better": True,
@@ -203,7 +233,7 @@ def bench_copy(args, dev):
             "config": {"workload": f"{args.component} of {unit_desc} of {args.workload}",
                        "bytes_per_launch": moved},
             "roofline": {"bound": bound, "achieved": round(gbs, 2), "peak": peak, "unit": "GB/s",
-                         "frac": round(gbs / peak, 4), "traffic": None,
+                         "frac": round(gbs / peak, 4), "traffic": traffic, "kernel": kernel,
                          "avg_launch_us": round(avg_ms * 1e3, 2), **extra},
             "cpu_baseline": None}
 
@@ -303,10 +333,12 @@ def main():
                     choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--component", default="pipeline",
-                    choices=("pipeline", "kv_write", "kv_offload", "decode", "control_plane"),
+                    choices=("pipeline", "kv_write", "kv_offload", "decode", "cascade_decode",
+                             "control_plane"),
                     help="pipeline (default): the serving step; kv_write / kv_offload: "
                          "the write-back scatter and the offload copy on their own; "
-                         "decode: paged decode attention (use --workload decode_batch); "
+                         "decode / cascade_decode: paged decode attention, per sequence or "
+                         "with each agent's anchor read once (use --workload decode_batch); "
                          "control_plane: the host-side scout on a synthetic agent trace")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a plain 1 GiB device-to-device copy (the reference kernel "
@@ -415,7 +447,7 @@ def main():
                                  "frac_link": round(iso_gbs / PEAK_PCIE5_X16_GBS, 4),
                                  "avg_launch_us": round(iso * 1e3, 2)}}
     khash = source_hash(KERNEL_SOURCES[:1])
-    traffic = load_traffic(args.workload, khash)
+    traffic = load_traffic("prefill_paged_attn_kernel<128>", args.workload, khash)
     result = {
         "metric": METRIC,
         "value": round(value, 2),

@@ -25,6 +25,8 @@
  *                            CPU tier (Sec. 4), the reverse of the prefetch.
  *   cs_paged_decode_attn   - one new token per sequence attends over its whole
  *                            paged KV (the decode that follows a prefill).
+ *   cs_cascade_decode_attn - the same decode with each agent's shared anchor
+ *                            attended once for all of its sequences.
  *
  * Conventions shared by all calls
  *   - Every pointer is caller-owned.  The GPU calls allocate no device or
@@ -187,6 +189,59 @@ int cs_paged_decode_attn(const void *q, const void *k_pool, const void *v_pool,
                          int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
                          int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                          int32_t block_size, float scale, void *out, cs_stream_t stream);
+
+/*
+ * Cascade (shared-prefix) decode: the same result as cs_paged_decode_attn,
+ * computed so that a prefix shared by a group of sequences is read once.
+ *
+ * Operation (Sec. 2.1, "Agent anchor": every invocation of an agent starts
+ * with the same prompt prefix; Sec. 2.2: anchor blocks are the most reused
+ * KV blocks, read by every invocation of the agent): the sequences are
+ * partitioned into num_groups groups of consecutive sequences, group g being
+ * sequences
+ * cu_groups[g] .. cu_groups[g+1]-1, whose first shared_lens[g] keys are the
+ * same pool blocks (identical block-table entries).  For each group and KV
+ * head the queries of all its sequences (and of the query heads of that KV
+ * head) are stacked and attend once over the shared keys, in chunks of 512
+ * keys; each chunk leaves a partial result (O relative to its running max m,
+ * m and the sum l) in the workspace.  Each sequence then attends its own keys
+ * shared_lens[g] .. seq_lens[r]-1 and merges all partials with log-sum-exp
+ * weights.  The output equals cs_paged_decode_attn's up to rounding order.
+ *
+ * Arguments (those of cs_paged_decode_attn, plus)
+ *   cu_groups       device, int32 [num_groups + 1]: 0 = cu_groups[0] <= ...
+ *                   <= cu_groups[num_groups] = batch.
+ *   shared_lens     device, int32 [num_groups]: multiples of 16, each at most
+ *                   max_shared_len and at most every seq_lens of its group
+ *                   (0: the group shares nothing).
+ *   num_groups      in [1, batch] (when batch > 0).
+ *   max_group_seqs  host bound on the sequences of a group with a nonzero
+ *                   shared_lens, in [1, batch] (groups sharing nothing may be
+ *                   larger).
+ *   max_shared_len  host bound on shared_lens, <= max_seq_len; sizes the launch
+ *                   and the workspace.
+ *   workspace       device, 16-byte aligned, caller-owned scratch of at least
+ *                   cs_cascade_decode_workspace_bytes(batch, num_q_heads,
+ *                   head_dim, max_shared_len) bytes (may be NULL when that is
+ *                   0); its contents are undefined after the call.  Calls that
+ *                   share a workspace must be ordered on one stream.
+ * With CS_DEBUG_CHECK=1 the group structure, the shared block ids and the
+ * decode metadata are validated on the host first.
+ */
+int cs_cascade_decode_attn(const void *q, const void *k_pool, const void *v_pool,
+                           const int32_t *block_tables, const int32_t *seq_lens, int32_t batch,
+                           int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
+                           const int32_t *cu_groups, const int32_t *shared_lens,
+                           int32_t num_groups, int32_t max_group_seqs, int32_t max_shared_len,
+                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                           int32_t block_size, float scale, void *workspace,
+                           int64_t workspace_bytes, void *out, cs_stream_t stream);
+
+/* Workspace bytes cs_cascade_decode_attn needs:
+ * ceil(max_shared_len / 512) * batch * num_q_heads * (head_dim + 2) * 4;
+ * -1 for a negative or zero size argument. */
+int64_t cs_cascade_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                          int32_t max_shared_len);
 
 /*
  * KV write-back: store the K/V rows of new tokens into their pool slots.

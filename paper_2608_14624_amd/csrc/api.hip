@@ -150,6 +150,40 @@ int debug_check_decode(const int32_t* block_tables, const int32_t* seq_lens, int
   return CS_OK;
 }
 
+// Groups partition the batch in order; each shared prefix is whole blocks
+// that every sequence of the group holds, through identical block ids.
+int debug_check_groups(const int32_t* block_tables, const int32_t* seq_lens,
+                       const int32_t* cu_groups, const int32_t* shared_lens, int batch,
+                       int num_groups, int max_group_seqs, int max_shared_len,
+                       int max_blocks_per_seq, hipStream_t stream) {
+  std::vector<int32_t> sl, bt, cu, sh;
+  hipError_t e = copy_to_host(sl, seq_lens, (size_t)batch, stream);
+  if (e == hipSuccess) e = copy_to_host(bt, block_tables, (size_t)batch * max_blocks_per_seq, stream);
+  if (e == hipSuccess) e = copy_to_host(cu, cu_groups, (size_t)num_groups + 1, stream);
+  if (e == hipSuccess) e = copy_to_host(sh, shared_lens, (size_t)num_groups, stream);
+  if (e != hipSuccess) return hip_fail(e, "CS_DEBUG_CHECK metadata copy");
+  if (cu[0] != 0 || cu[num_groups] != batch)
+    return fail(CS_ERR_INVALID_ARG, "cu_groups must start at 0 and end at batch = %d", batch);
+  for (int g = 0; g < num_groups; ++g) {
+    const int n = cu[g + 1] - cu[g];
+    if (n < 0) return fail(CS_ERR_INVALID_ARG, "cu_groups decreases at %d", g);
+    if (sh[g] > 0 && n > max_group_seqs)
+      return fail(CS_ERR_INVALID_ARG, "group %d has %d sequences (max_group_seqs %d)", g, n, max_group_seqs);
+    if (sh[g] < 0 || sh[g] % 16 != 0 || sh[g] > max_shared_len)
+      return fail(CS_ERR_INVALID_ARG, "shared_lens[%d] = %d is not a multiple of 16 in [0, %d]", g,
+                  sh[g], max_shared_len);
+    for (int r = cu[g]; r < cu[g + 1]; ++r) {
+      if (sh[g] > sl[r])
+        return fail(CS_ERR_INVALID_ARG, "shared_lens[%d] = %d exceeds seq_lens[%d] = %d", g, sh[g], r, sl[r]);
+      for (int b = 0; b < sh[g] / 16; ++b) {
+        if (bt[(size_t)r * max_blocks_per_seq + b] != bt[(size_t)cu[g] * max_blocks_per_seq + b])
+          return fail(CS_ERR_INVALID_ARG, "sequence %d does not share block %d of group %d", r, b, g);
+      }
+    }
+  }
+  return CS_OK;
+}
+
 // Device-visible address of a pinned, device-mapped host buffer, or null.
 const void* mapped_host_pointer(const void* host, const char* name, int* status) {
   hipPointerAttribute_t attr;
@@ -168,6 +202,46 @@ const void* mapped_host_pointer(const void* host, const char* name, int* status)
   const char* base_d = static_cast<const char*>(attr.devicePointer);
   *status = CS_OK;
   return base_d + (static_cast<const char*>(host) - base_h);
+}
+
+}  // namespace
+
+namespace {
+
+// Argument checks shared by the decode calls; *noop is set for an empty batch.
+int validate_decode(const void* q, const void* k_pool, const void* v_pool,
+                    const int32_t* block_tables, const int32_t* seq_lens, int32_t batch,
+                    int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
+                    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                    int32_t block_size, float scale, const void* out, bool* noop) {
+  *noop = false;
+  if (batch < 0 || max_seq_len < 0 || max_blocks_per_seq < 0 || num_blocks < 0)
+    return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+    return fail(CS_ERR_INVALID_ARG, "head counts, head_dim and block_size must be positive");
+  if (num_q_heads % num_kv_heads != 0)
+    return fail(CS_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                num_q_heads, num_kv_heads);
+  if (num_q_heads / num_kv_heads > 16)
+    return fail(CS_ERR_UNSUPPORTED, "more than 16 query heads per KV head");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
+  if (!isfinite(scale)) return fail(CS_ERR_INVALID_ARG, "scale is not finite");
+  if (batch == 0) {
+    *noop = true;
+    return CS_OK;
+  }
+  if (!q || !k_pool || !v_pool || !block_tables || !seq_lens || !out)
+    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  if (num_blocks == 0 || max_seq_len == 0)
+    return fail(CS_ERR_INVALID_ARG, "num_blocks and max_seq_len must be positive");
+  if ((long long)max_blocks_per_seq * block_size < max_seq_len)
+    return fail(CS_ERR_INVALID_ARG, "max_blocks_per_seq * block_size < max_seq_len");
+  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool))
+    return fail(CS_ERR_INVALID_ARG, "q, k_pool and v_pool must be 16-byte aligned");
+  if ((long long)batch * num_kv_heads > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
+  return CS_OK;
 }
 
 }  // namespace
@@ -290,29 +364,12 @@ int cs_paged_decode_attn(const void* q, const void* k_pool, const void* v_pool,
                          int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
                          int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                          int32_t block_size, float scale, void* out, cs_stream_t stream) {
-  if (batch < 0 || max_seq_len < 0 || max_blocks_per_seq < 0 || num_blocks < 0)
-    return fail(CS_ERR_INVALID_ARG, "negative size argument");
-  if (num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
-    return fail(CS_ERR_INVALID_ARG, "head counts, head_dim and block_size must be positive");
-  if (num_q_heads % num_kv_heads != 0)
-    return fail(CS_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d",
-                num_q_heads, num_kv_heads);
-  if (num_q_heads / num_kv_heads > 16)
-    return fail(CS_ERR_UNSUPPORTED, "more than 16 query heads per KV head");
-  if (head_dim != 64 && head_dim != 128)
-    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
-  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
-  if (!isfinite(scale)) return fail(CS_ERR_INVALID_ARG, "scale is not finite");
-  if (batch == 0) return ok();
-  if (!q || !k_pool || !v_pool || !block_tables || !seq_lens || !out)
-    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
-  if (num_blocks == 0 || max_seq_len == 0)
-    return fail(CS_ERR_INVALID_ARG, "num_blocks and max_seq_len must be positive");
-  if ((long long)max_blocks_per_seq * block_size < max_seq_len)
-    return fail(CS_ERR_INVALID_ARG, "max_blocks_per_seq * block_size < max_seq_len");
-  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool))
-    return fail(CS_ERR_INVALID_ARG, "q, k_pool and v_pool must be 16-byte aligned");
-  if ((long long)batch * num_kv_heads > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
+  bool noop;
+  int st0 = validate_decode(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
+                            max_blocks_per_seq, num_blocks, num_q_heads, num_kv_heads, head_dim,
+                            block_size, scale, out, &noop);
+  if (st0 != CS_OK) return st0;
+  if (noop) return ok();
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (debug_checks_enabled()) {
     int st = debug_check_decode(block_tables, seq_lens, batch, max_seq_len, max_blocks_per_seq,
@@ -334,6 +391,84 @@ int cs_paged_decode_attn(const void* q, const void* k_pool, const void* v_pool,
   a.scale = scale;
   hipError_t e = cs::launch_paged_decode_attn(a, s);
   if (e != hipSuccess) return hip_fail(e, "paged_decode_attn launch");
+  return ok();
+}
+
+int64_t cs_cascade_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t head_dim,
+                                           int32_t max_shared_len) {
+  if (batch < 0 || num_q_heads <= 0 || head_dim <= 0 || max_shared_len < 0) return -1;
+  const long long chunk = (long long)cs::kCascadeChunkSteps * 64;
+  const long long chunks = (max_shared_len + chunk - 1) / chunk;
+  return (int64_t)(chunks * batch * num_q_heads * (head_dim + 2) * (long long)sizeof(float));
+}
+
+int cs_cascade_decode_attn(const void* q, const void* k_pool, const void* v_pool,
+                           const int32_t* block_tables, const int32_t* seq_lens, int32_t batch,
+                           int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
+                           const int32_t* cu_groups, const int32_t* shared_lens,
+                           int32_t num_groups, int32_t max_group_seqs, int32_t max_shared_len,
+                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                           int32_t block_size, float scale, void* workspace,
+                           int64_t workspace_bytes, void* out, cs_stream_t stream) {
+  bool noop;
+  int st0 = validate_decode(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
+                            max_blocks_per_seq, num_blocks, num_q_heads, num_kv_heads, head_dim,
+                            block_size, scale, out, &noop);
+  if (st0 != CS_OK) return st0;
+  if (num_groups < 0 || max_group_seqs < 0 || max_shared_len < 0 || workspace_bytes < 0)
+    return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (noop) return ok();
+  if (num_groups < 1 || num_groups > batch)
+    return fail(CS_ERR_INVALID_ARG, "num_groups %d outside [1, batch = %d]", num_groups, batch);
+  if (max_group_seqs < 1 || max_group_seqs > batch)
+    return fail(CS_ERR_INVALID_ARG, "max_group_seqs %d outside [1, batch = %d]", max_group_seqs, batch);
+  if (max_shared_len > max_seq_len)
+    return fail(CS_ERR_INVALID_ARG, "max_shared_len %d exceeds max_seq_len %d", max_shared_len, max_seq_len);
+  if (!cu_groups || !shared_lens) return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  const int64_t need = cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim, max_shared_len);
+  if (need > 0) {
+    if (!workspace || !aligned16(workspace))
+      return fail(CS_ERR_INVALID_ARG, "workspace must be a 16-byte aligned device buffer");
+    if (workspace_bytes < need)
+      return fail(CS_ERR_INVALID_ARG, "workspace_bytes %lld < %lld required", (long long)workspace_bytes,
+                  (long long)need);
+  }
+  const cs::CascadeGeometry geo = cs::cascade_geometry(num_groups, max_group_seqs, max_shared_len,
+                                                       num_q_heads, num_kv_heads);
+  if (geo.grid > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (debug_checks_enabled()) {
+    int st = debug_check_decode(block_tables, seq_lens, batch, max_seq_len, max_blocks_per_seq,
+                                num_blocks, s);
+    if (st == CS_OK)
+      st = debug_check_groups(block_tables, seq_lens, cu_groups, shared_lens, batch, num_groups,
+                              max_group_seqs, max_shared_len, max_blocks_per_seq, s);
+    if (st != CS_OK) return st;
+  }
+  cs::CascadeLaunch a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_tables = block_tables;
+  a.seq_lens = seq_lens;
+  a.cu_groups = cu_groups;
+  a.shared_lens = shared_lens;
+  a.out = static_cast<uint16_t*>(out);
+  a.ws_o = static_cast<float*>(workspace);
+  a.ws_ml = a.ws_o + (size_t)geo.chunks * batch * num_q_heads * head_dim;
+  a.batch = batch;
+  a.max_blocks_per_seq = max_blocks_per_seq;
+  a.num_groups = num_groups;
+  a.max_group_seqs = max_group_seqs;
+  a.max_shared_len = max_shared_len;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.scale = scale;
+  hipError_t e = cs::launch_shared_prefix_partials(a, s);
+  if (e != hipSuccess) return hip_fail(e, "shared-prefix attention launch");
+  e = cs::launch_cascade_decode_rest(a, s);
+  if (e != hipSuccess) return hip_fail(e, "cascade decode launch");
   return ok();
 }
 

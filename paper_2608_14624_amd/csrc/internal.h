@@ -91,4 +91,46 @@ struct DecodeLaunch {
 
 hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream);
 
+// Cascade decode: the shared prefix of each group of sequences is attended
+// once with the group's queries stacked (prefill kernel, stacked mode), in
+// chunks of kCascadeChunkSteps * 64 keys whose partial results go to a
+// workspace; the decode kernel then attends each sequence's own keys and
+// merges the partials.
+constexpr int kCascadeChunkSteps = 8;
+
+struct CascadeGeometry {
+  int chunk_keys;     // keys per chunk of a shared prefix
+  int chunks;         // chunks of the longest shared prefix
+  int row_tiles;      // 128-row tiles of the largest group
+  long long grid;     // work-groups of the shared-prefix launch
+};
+
+CascadeGeometry cascade_geometry(int num_groups, int max_group_seqs, int max_shared_len,
+                                 int num_q_heads, int num_kv_heads);
+
+struct CascadeLaunch {
+  const uint16_t* q;        // [batch][num_q_heads][head_dim]
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_tables;
+  const int32_t* seq_lens;
+  const int32_t* cu_groups;     // [num_groups + 1]
+  const int32_t* shared_lens;   // [num_groups]
+  uint16_t* out;
+  float* ws_o;                  // [chunks][batch * num_q_heads][head_dim]
+  float* ws_ml;                 // [chunks][batch * num_q_heads][2]
+  int batch;
+  int max_blocks_per_seq;
+  int num_groups;
+  int max_group_seqs;
+  int max_shared_len;
+  int num_q_heads;
+  int num_kv_heads;
+  int head_dim;
+  float scale;
+};
+
+hipError_t launch_shared_prefix_partials(const CascadeLaunch& a, hipStream_t stream);
+hipError_t launch_cascade_decode_rest(const CascadeLaunch& a, hipStream_t stream);
+
 }  // namespace cs

@@ -23,6 +23,13 @@
 //   * The K/V loads of a wave's next chunk are issued before the math of the
 //     current one, so each wave keeps 16 KiB in flight.
 //   * Work-groups are ordered KV head fastest, so each XCD serves one head.
+//
+// Cascade mode: a sequence belongs to a group whose shared prefix (its first
+// shared_len keys) was already attended by the stacked prefill kernel, which
+// left one partial result (O relative to its running max m, the max m and
+// the sum l) per 512-key chunk in a workspace.  The kernel then attends only
+// the sequence's own keys shared_len .. L - 1 and merges those partials with
+// its four waves' ones, all with log-sum-exp weights exp2((m_i - max) * c).
 #include "internal.h"
 
 #include <math.h>
@@ -55,6 +62,14 @@ struct DecParams {
   int num_kv_heads;
   int group;
   float scale_log2;
+  // cascade mode only
+  const int32_t* cu_groups;     // [num_groups + 1], cu_groups[0] = 0, last = batch
+  const int32_t* shared_lens;   // [num_groups]
+  int num_groups;
+  int chunk_keys;               // keys per partial of the shared prefix
+  const float* ws_o;            // [chunks][batch * num_q_heads][D]
+  const float* ws_ml;           // [chunks][batch * num_q_heads][2]
+  int ws_rows;
 };
 
 template <int D>
@@ -74,7 +89,7 @@ struct DecLds {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-template <int D>
+template <int D, bool kCascade>
 __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p) {
   __shared__ DecLds<D> sm;
   constexpr int vStride = DecLds<D>::vStride;
@@ -93,6 +108,22 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
   const int L = p.seq_lens[r];
   const int n_blk = (L + kBlock - 1) / kBlock;
   const int n_chunks = (L + kChunk - 1) / kChunk;
+  int start = 0;       // first key this kernel attends
+  int n_parts = 0;     // partial results of the shared prefix to merge
+  if constexpr (kCascade) {
+    // the sequence's group: the last gr with cu_groups[gr] <= r
+    int lo = 0, hi = p.num_groups - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (p.cu_groups[mid] <= r) lo = mid; else hi = mid - 1;
+    }
+    start = p.shared_lens[lo];
+    n_parts = (start + p.chunk_keys - 1) / p.chunk_keys;
+  }
+  const int first_chunk = start / kChunk;
+  // no chunk when the shared prefix covers the whole sequence (a chunk with
+  // no visible key would turn the running max into -inf - -inf)
+  const int ch_end = start < L ? n_chunks : first_chunk;
   const size_t tile_elems = (size_t)kBlock * D;
   const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
   const uint16_t* kbase = p.k_pool + (size_t)g * tile_elems;
@@ -163,9 +194,9 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
   float l_run = 0.f;
   const float c = p.scale_log2;
 
-  int ch = wave;
-  if (ch < n_chunks) load_chunk(ch);
-  for (; ch < n_chunks; ch += kWaves) {
+  int ch = first_chunk + wave;
+  if (ch < ch_end) load_chunk(ch);
+  for (; ch < ch_end; ch += kWaves) {
     // V rows of this chunk into the wave's LDS tile
 #pragma unroll
     for (int u = 0; u < kVLoads; ++u) {
@@ -179,7 +210,7 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
 #pragma unroll
       for (int dc = 0; dc < DC; ++dc)
         s[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kreg[mt][dc]), qreg[dc], s[mt], 0, 0, 0);
-    if (ch + kWaves < n_chunks) load_chunk(ch + kWaves);   // in flight during the math
+    if (ch + kWaves < ch_end) load_chunk(ch + kWaves);     // in flight during the math
 
     // mask keys past the end; register r of tile mt holds key 32*ch + 16*mt + 4*qd + r
     const int kbase_idx = ch * kChunk;
@@ -189,7 +220,7 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int key = kbase_idx + 16 * mt + 4 * qd + rr;
-        s[mt][rr] = key < L ? s[mt][rr] : -INFINITY;
+        s[mt][rr] = (key < L && key >= start) ? s[mt][rr] : -INFINITY;
         mloc = fmaxf(mloc, s[mt][rr]);
       }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
@@ -233,9 +264,11 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
   for (int idx = threadIdx.x; idx < p.group * D; idx += kThreads) {
     const int hj = idx / D;
     const int d = idx % D;
+    const size_t row = (size_t)r * p.num_q_heads + g * p.group + hj;
     float mx = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, sm.merge.m[w][hj]);
+    for (int pc = 0; pc < n_parts; ++pc) mx = fmaxf(mx, p.ws_ml[2 * ((size_t)pc * p.ws_rows + row)]);
     float num = 0.f, den = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
@@ -243,8 +276,13 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
       num += wt * sm.merge.o[w][hj][d];
       den += wt * sm.merge.l[w][hj];
     }
-    p.out[((size_t)r * p.num_q_heads + g * p.group + hj) * D + d] =
-        __builtin_bit_cast(uint16_t, (__bf16)(num / den));
+    for (int pc = 0; pc < n_parts; ++pc) {
+      const size_t widx = (size_t)pc * p.ws_rows + row;
+      const float wt = __builtin_amdgcn_exp2f((p.ws_ml[2 * widx] - mx) * c);
+      num += wt * p.ws_o[widx * D + d];
+      den += wt * p.ws_ml[2 * widx + 1];
+    }
+    p.out[row * D + d] = __builtin_bit_cast(uint16_t, (__bf16)(num / den));
   }
 }
 
@@ -265,9 +303,38 @@ hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream) {
   p.scale_log2 = a.scale * kLog2e;
   const dim3 grid((unsigned)((long long)a.batch * a.num_kv_heads)), block(kThreads);
   if (a.head_dim == 128) {
-    hipLaunchKernelGGL(paged_decode_attn_kernel<128>, grid, block, 0, stream, p);
+    hipLaunchKernelGGL((paged_decode_attn_kernel<128, false>), grid, block, 0, stream, p);
   } else {
-    hipLaunchKernelGGL(paged_decode_attn_kernel<64>, grid, block, 0, stream, p);
+    hipLaunchKernelGGL((paged_decode_attn_kernel<64, false>), grid, block, 0, stream, p);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_cascade_decode_rest(const CascadeLaunch& a, hipStream_t stream) {
+  DecParams p = {};
+  p.q = a.q;
+  p.k_pool = a.k_pool;
+  p.v_pool = a.v_pool;
+  p.block_tables = a.block_tables;
+  p.seq_lens = a.seq_lens;
+  p.out = a.out;
+  p.max_blocks_per_seq = a.max_blocks_per_seq;
+  p.num_q_heads = a.num_q_heads;
+  p.num_kv_heads = a.num_kv_heads;
+  p.group = a.num_q_heads / a.num_kv_heads;
+  p.scale_log2 = a.scale * kLog2e;
+  p.cu_groups = a.cu_groups;
+  p.shared_lens = a.shared_lens;
+  p.num_groups = a.num_groups;
+  p.chunk_keys = kCascadeChunkSteps * 64;
+  p.ws_o = a.ws_o;
+  p.ws_ml = a.ws_ml;
+  p.ws_rows = a.batch * a.num_q_heads;
+  const dim3 grid((unsigned)((long long)a.batch * a.num_kv_heads)), block(kThreads);
+  if (a.head_dim == 128) {
+    hipLaunchKernelGGL((paged_decode_attn_kernel<128, true>), grid, block, 0, stream, p);
+  } else {
+    hipLaunchKernelGGL((paged_decode_attn_kernel<64, true>), grid, block, 0, stream, p);
   }
   return hipGetLastError();
 }

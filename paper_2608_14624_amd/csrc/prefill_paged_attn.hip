@@ -18,10 +18,11 @@
 //     online softmax are in-lane reductions plus one exchange between the two
 //     lane halves, and the probabilities leave the S^T accumulator already in
 //     the register layout of the B operand of the PV product.
-//   * Keys are consumed 64 at a time (4 pool blocks).  K is staged row-major
-//     [key][d]; V is staged transposed [d][key] so that the A operand of the
-//     PV product is two 8-byte LDS reads.  Rows are padded to spread LDS
-//     banks.  Block ids are read from the block table per 16-token block.
+//   * Keys are consumed 64 at a time (4 pool blocks, one staged by each
+//     wave).  K and V are both staged row-major [key][d]; the A operand of
+//     the PV product (V^T) comes from two transposing 8-byte LDS reads
+//     (ds_read_b64_tr_b16).  Rows are padded to spread LDS banks.  Block ids
+//     are read from the block table per 16-token block.
 //   * Masking is a select to -inf (never an additive mask), so positions past
 //     the end of a sequence inside its last block never contribute whatever
 //     they hold; whole blocks past the end are zero-filled in LDS, never read.
@@ -30,6 +31,14 @@
 // Work-group order: the KV head varies fastest, so with 8 KV heads the 8 XCDs
 // each serve one KV head and its K/V stays in that XCD's L2; token tiles are
 // issued from the last (most keys) to the first.
+//
+// Stacked mode (the shared-prefix half of cascade attention): the query rows
+// of a work-group are any 128 (sequence, query head) pairs of one group of
+// sequences that share a prefix and one KV head; they attend, without a
+// causal limit, over one 64-key-aligned chunk of the shared prefix, and the
+// work-group writes its unnormalized partial result (O, running max m, sum
+// l) to a workspace instead of the output.  The other half (each sequence's
+// own keys) and the log-sum-exp merge run in the decode kernel.
 #include "internal.h"
 
 #include <math.h>
@@ -69,6 +78,15 @@ struct Params {
   int token_tiles;
   int head_tiles;
   float scale_log2;   // scale * log2(e)
+  // stacked mode only
+  const int32_t* cu_groups;     // [num_groups + 1] sequence range of each group
+  const int32_t* shared_lens;   // [num_groups] shared prefix tokens (multiple of 16)
+  int row_tiles;                // 128-row tiles of the largest group
+  int chunk_steps;              // 64-key steps per chunk of the shared prefix
+  int chunks;                   // chunks of the longest shared prefix
+  float* ws_o;                  // [chunks][batch * num_q_heads][D] partial O
+  float* ws_ml;                 // [chunks][batch * num_q_heads][2] partial (m, l)
+  int ws_rows;                  // batch * num_q_heads
 };
 
 template <int D>
@@ -108,7 +126,9 @@ __device__ __forceinline__ float pair_sum(float x) {
   return a + b;
 }
 
-template <int D>
+constexpr int kRowsPerWG = kNQ * kWaves;
+
+template <int D, bool kStacked>
 __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) {
   __shared__ Lds<D> sm;
   constexpr int kStride = Lds<D>::kStride;
@@ -125,38 +145,78 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   // ---- work tile -----------------------------------------------------
   // Work-groups are dealt to the 8 XCDs round-robin, so the KV head is the
   // fastest-varying index: with 8 KV heads every XCD serves exactly one and
-  // keeps its K/V in its own L2.  The head tiles of that KV head come next,
-  // then invocations, then token tiles from the last (most keys) to the first.
+  // keeps its K/V in its own L2.
   const int wg = blockIdx.x;
-  const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
-  const int g = wg % p.num_kv_heads;
-  const int sub = wg / p.num_kv_heads;
-  const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
-  const int rest = sub / tiles_per_kv;
-  const int r = rest % p.batch;
-  const int token_tile = p.token_tiles - 1 - rest / p.batch;
-  const int q0 = p.cu_q_lens[r];
-  const int S = p.cu_q_lens[r + 1] - q0;
-  const int t0 = token_tile * p.span;
-  if (t0 >= S) return;
-  const int P = p.prefix_lens[r];
-  const int L = P + S;
-
-  const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
-  const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
-  const bool row_valid = t < S;
-  const int qpos = row_valid ? P + t : L - 1;              // last visible key
-  const int kv_end = P + min(S, t0 + p.span);              // keys the tile needs
-  const int n_steps = (kv_end + kBN - 1) / kBN;
-  const int n_blk = (L + kBlock - 1) / kBlock;
-  const int32_t* bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
+  int g;                // KV head
+  bool row_valid;       // this lane holds a real query row
+  size_t qrow;          // element offset of the row in q (and out)
+  int qpos;             // last key the row sees
+  int j0;               // first 64-key step
+  int n_steps;          // steps of the work-group
+  int n_blk;            // blocks of the key range reached through bt
+  int wave_qmin;        // first key position some row of this wave cannot see
+  const int32_t* bt;
+  int chunk = 0;
+  if constexpr (!kStacked) {
+    // the head tiles of the KV head come next, then invocations, then
+    // token tiles from the last (most keys) to the first
+    const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
+    g = wg % p.num_kv_heads;
+    const int sub = wg / p.num_kv_heads;
+    const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
+    const int rest = sub / tiles_per_kv;
+    const int r = rest % p.batch;
+    const int token_tile = p.token_tiles - 1 - rest / p.batch;
+    const int q0 = p.cu_q_lens[r];
+    const int S = p.cu_q_lens[r + 1] - q0;
+    const int t0 = token_tile * p.span;
+    if (t0 >= S) return;
+    const int P = p.prefix_lens[r];
+    const int L = P + S;
+    const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
+    const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
+    row_valid = t < S;
+    qrow = ((size_t)(q0 + (row_valid ? t : 0)) * p.num_q_heads + h) * D;
+    qpos = row_valid ? P + t : L - 1;
+    const int kv_end = P + min(S, t0 + p.span);              // keys the tile needs
+    j0 = 0;
+    n_steps = (kv_end + kBN - 1) / kBN;
+    n_blk = (L + kBlock - 1) / kBlock;
+    bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
+    wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
+  } else {
+    // then row tiles, chunks of the shared prefix, groups
+    g = wg % p.num_kv_heads;
+    int rest = wg / p.num_kv_heads;
+    const int rt = rest % p.row_tiles;
+    rest /= p.row_tiles;
+    chunk = rest % p.chunks;
+    const int gr = rest / p.chunks;
+    const int s0 = p.cu_groups[gr];
+    const int n_rows = (p.cu_groups[gr + 1] - s0) * p.group;
+    const int SH = p.shared_lens[gr];
+    const int kb = chunk * p.chunk_steps * kBN;
+    if (rt * kRowsPerWG >= n_rows || kb >= SH) return;
+    const int ke = min(SH, kb + p.chunk_steps * kBN);
+    const int rho = rt * kRowsPerWG + wave * kNQ + qi;
+    row_valid = rho < n_rows;
+    const int rr = row_valid ? rho : 0;
+    const int seq = s0 + rr / p.group;
+    const int h = g * p.group + rr % p.group;
+    qrow = ((size_t)seq * p.num_q_heads + h) * D;
+    qpos = ke - 1;
+    j0 = kb / kBN;
+    n_steps = (ke - kb + kBN - 1) / kBN;
+    n_blk = SH / kBlock;
+    bt = p.block_tables + (size_t)s0 * p.max_blocks_per_seq;   // the group's shared blocks
+    wave_qmin = ke - 1;
+  }
   const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
   const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
   const uint16_t* kbase = p.k_pool + (size_t)g * tile_elems;
   const uint16_t* vbase = p.v_pool + (size_t)g * tile_elems;
 
   // ---- Q^T operand: lane holds query qi, dims ks*16 + half*8 .. +7 -----
-  const size_t qrow = ((size_t)(q0 + t) * p.num_q_heads + h) * D;
   bf16x8 qreg[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
@@ -176,7 +236,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   const __attribute__((address_space(4))) int32_t* bt_c =
       (const __attribute__((address_space(4))) int32_t*)bt;
   auto block_id = [&](int step) -> int {
-    const int lb = step * (kBN / kBlock) + wave_u;
+    const int lb = (j0 + step) * (kBN / kBlock) + wave_u;
     return lb < n_blk ? bt_c[lb] : -1;                               // -1: past the end
   };
 
@@ -247,8 +307,6 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
   float m_run = -INFINITY;     // running max of the raw (unscaled) logits
   const float c = p.scale_log2;
-  // first key position that some row of this wave cannot see
-  const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
 
   // ---- prologue: step 0 in LDS buffer 0; steps 1 and 2 in registers ----
   float l_part[4] = {0.f, 0.f, 0.f, 0.f};     // partial row sums (short add chains)
@@ -274,7 +332,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   // One step: stage j+1 into LDS, issue the loads of step j+3, then the
   // logits, softmax and PV product of step j.
   auto step = [&](const int j, Stage& kst, Stage& vst) {
-    const int kstart = j * kBN;
+    const int kstart = (j0 + j) * kBN;
     const int cur = j & 1;
     __syncthreads();   // iteration j-1's reads are done and its writes visible
     if (j + 1 < n_steps) {
@@ -368,8 +426,26 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   }
   const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
 
-  // ---- epilogue: O / l, bf16, store --------------------------------
   const float l_tot = pair_sum(l_run);
+  if constexpr (kStacked) {
+    // ---- partial result: O (relative to m_run), m_run, l -----------
+    if (row_valid) {
+      const size_t widx = (size_t)chunk * p.ws_rows + qrow / D;
+      float* orow = p.ws_o + widx * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const float4 o = make_float4(oacc[dt][rg * 4], oacc[dt][rg * 4 + 1], oacc[dt][rg * 4 + 2],
+                                       oacc[dt][rg * 4 + 3]);
+          *reinterpret_cast<float4*>(orow + dt * 32 + 8 * rg + 4 * half) = o;
+        }
+      }
+      if (half == 0) *reinterpret_cast<float2*>(p.ws_ml + 2 * widx) = make_float2(m_run, l_tot);
+    }
+    return;
+  }
+  // ---- epilogue: O / l, bf16, store --------------------------------
   const float inv = 1.f / l_tot;
   if (row_valid) {
     uint16_t* orow = p.out + qrow;
@@ -421,9 +497,52 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
   p.scale_log2 = a.scale * kLog2e;
   const dim3 grid((unsigned)geo.grid), block(kThreads);
   if (a.head_dim == 128) {
-    hipLaunchKernelGGL(prefill_paged_attn_kernel<128>, grid, block, 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, false>), grid, block, 0, stream, p);
   } else {
-    hipLaunchKernelGGL(prefill_paged_attn_kernel<64>, grid, block, 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, false>), grid, block, 0, stream, p);
+  }
+  return hipGetLastError();
+}
+
+CascadeGeometry cascade_geometry(int num_groups, int max_group_seqs, int max_shared_len,
+                                 int num_q_heads, int num_kv_heads) {
+  CascadeGeometry geo;
+  const int group = num_q_heads / num_kv_heads;
+  geo.chunk_keys = kCascadeChunkSteps * kBN;
+  geo.chunks = (max_shared_len + geo.chunk_keys - 1) / geo.chunk_keys;
+  geo.row_tiles = ((long long)max_group_seqs * group + kRowsPerWG - 1) / kRowsPerWG;
+  geo.grid = (long long)num_kv_heads * geo.row_tiles * geo.chunks * num_groups;
+  return geo;
+}
+
+hipError_t launch_shared_prefix_partials(const CascadeLaunch& a, hipStream_t stream) {
+  const CascadeGeometry geo = cascade_geometry(a.num_groups, a.max_group_seqs, a.max_shared_len,
+                                               a.num_q_heads, a.num_kv_heads);
+  if (geo.grid == 0) return hipSuccess;
+  Params p = {};
+  p.q = a.q;
+  p.k_pool = a.k_pool;
+  p.v_pool = a.v_pool;
+  p.block_tables = a.block_tables;
+  p.batch = a.batch;
+  p.max_blocks_per_seq = a.max_blocks_per_seq;
+  p.num_q_heads = a.num_q_heads;
+  p.num_kv_heads = a.num_kv_heads;
+  p.group = a.num_q_heads / a.num_kv_heads;
+  p.scale_log2 = a.scale * kLog2e;
+  p.cu_groups = a.cu_groups;
+  p.shared_lens = a.shared_lens;
+  p.row_tiles = geo.row_tiles;
+  p.chunk_steps = kCascadeChunkSteps;
+  p.chunks = geo.chunks;
+  p.ws_o = a.ws_o;
+  p.ws_ml = a.ws_ml;
+  p.ws_rows = a.batch * a.num_q_heads;
+  const dim3 grid((unsigned)geo.grid), block(kThreads);
+  if (a.head_dim == 128) {
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, true>), grid, block, 0, stream, p);
+  } else {
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, true>), grid, block, 0, stream, p);
   }
   return hipGetLastError();
 }

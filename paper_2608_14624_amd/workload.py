@@ -447,6 +447,42 @@ def decode_view(wl):
     return np.ascontiguousarray(wl.q[last]), wl.kv_lens.astype(np.int32)
 
 
+def cascade_view(wl):
+    """The decode batch of ``wl`` ordered for cascade attention.
+
+    Sequences of an agent with a prefix hit share the anchor's full blocks
+    (the same pool slots); they become one group whose shared length is those
+    blocks' tokens.  Sequences without a hit form one last group sharing
+    nothing.  Returns a dict with ``order`` (the batch permutation: row ``i``
+    of the grouped batch is sequence ``order[i]``), ``cu_groups``,
+    ``shared_lens``, ``max_group_seqs`` (over groups that share something, at
+    least 1) and ``max_shared_len``.
+    """
+    bs = wl.block_size
+    by_agent = {}
+    misses = []
+    for r, inv in enumerate(wl.invocations):
+        if inv.hit and wl.anchor_lens[inv.agent] >= bs:
+            by_agent.setdefault(inv.agent, []).append(r)
+        else:
+            misses.append(r)
+    order, cu, shared = [], [0], []
+    for a in sorted(by_agent):
+        order += by_agent[a]
+        cu.append(len(order))
+        shared.append(wl.anchor_lens[a] // bs * bs)
+    if misses:
+        order += misses
+        cu.append(len(order))
+        shared.append(0)
+    sizes = [cu[i + 1] - cu[i] for i in range(len(shared)) if shared[i] > 0]
+    return dict(order=np.asarray(order, dtype=np.int64),
+                cu_groups=np.asarray(cu, dtype=np.int32),
+                shared_lens=np.asarray(shared, dtype=np.int32),
+                max_group_seqs=max(sizes + [1]),
+                max_shared_len=max(shared + [0]))
+
+
 def make_config(name):
     """Build the named configuration's arrays."""
     spec = config_spec(name)

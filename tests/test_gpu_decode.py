@@ -86,3 +86,139 @@ def test_decode_batch_config():
     err = np.abs(got - ref)
     print(f"    max_abs={err.max():.3e} mean_abs={err.mean():.3e}", flush=True)
     assert np.isfinite(got).all() and err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
+
+
+# ---------------------------------------------------------------- cascade decode
+
+def oracle_decode(q, seq_lens, block_tables, wl):
+    """The oracle for a decode batch: query r is position seq_lens[r] - 1 and
+    sees keys 0 .. seq_lens[r] - 1 (a one-token suffix after a prefix of
+    seq_lens[r] - 1 tokens)."""
+    b = len(seq_lens)
+    samples = [(r, h, 0) for r in range(b) for h in range(wl.num_q_heads)]
+    ref = oracle.prefill_paged_attn_rows(q, wl.k_pool, wl.v_pool, block_tables,
+                                         np.asarray(seq_lens, np.int32) - 1,
+                                         np.arange(b + 1, dtype=np.int32), wl.num_q_heads,
+                                         wl.num_kv_heads, wl.scale, samples)
+    return ref.reshape(b, wl.num_q_heads, -1)
+
+
+def grouped_batch(wl):
+    from paper_2608_14624_amd.workload import cascade_view
+    cv = cascade_view(wl)
+    q, seq_lens = decode_view(wl)
+    o = cv["order"]
+    return (np.ascontiguousarray(q[o]), np.ascontiguousarray(seq_lens[o]),
+            np.ascontiguousarray(wl.block_tables[o]), cv)
+
+
+def run_cascade(wl, q, seq_lens, bt, cu, shared, max_group_seqs, max_shared_len, workspace=None):
+    from paper_2608_14624_amd import ops
+    qd = dev_bf16(q)
+    out = torch.full_like(qd, float("nan"))
+    ops.cs_cascade_decode_attn(qd, dev_bf16(wl.k_pool), dev_bf16(wl.v_pool),
+                               torch.from_numpy(bt).cuda(), torch.from_numpy(seq_lens).cuda(),
+                               torch.from_numpy(np.asarray(cu, np.int32)).cuda(),
+                               torch.from_numpy(np.asarray(shared, np.int32)).cuda(), out,
+                               max_seq_len=int(seq_lens.max()), max_group_seqs=max_group_seqs,
+                               max_shared_len=max_shared_len, scale=wl.scale, workspace=workspace)
+    torch.cuda.synchronize()
+    return oracle.bf16_bits_to_f64(out.view(torch.int16).cpu().numpy().view(np.uint16))
+
+
+def check(got, ref, what):
+    err = np.abs(got - ref)
+    print(f"    {what}: max_abs={err.max():.3e} mean_abs={err.mean():.3e}", flush=True)
+    assert np.isfinite(got).all() and err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
+
+
+CASCADE_CASES = {
+    # name: (anchors, [(agent, suffix, hit)], Hq, Hkv, D)
+    # shared prefixes of 1 .. 3 chunks with ragged tails, a miss group, an
+    # anchor shorter than one block (shares nothing)
+    "mixed_g4": ([1100, 530, 8, 700], [(0, 3, True), (1, 40, True), (0, 1, True), (2, 5, True),
+                                      (1, 200, True), (3, 17, False), (0, 64, True),
+                                      (3, 9, True)], 32, 8, 128),
+    "mha_d64": ([600], [(0, 1, True), (0, 30, True)], 4, 4, 64),
+    "group16": ([520], [(0, 2, True), (0, 3, True)], 32, 2, 128),
+    "group8_d64": ([1030, 96], [(1, 5, True), (0, 7, True), (1, 1, True), (0, 90, True)], 16, 2, 64),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASCADE_CASES))
+def test_cascade_decode_matches_oracle(name):
+    anchors, spec, hq, hkv, d = CASCADE_CASES[name]
+    invs = [Invocation(a, s, h) for a, s, h in spec]
+    wl = build_workload(name, 41, anchors, invs, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                        num_blocks=1024)
+    q, seq_lens, bt, cv = grouped_batch(wl)
+    print(f"[case] cascade {name}: cu={cv['cu_groups'].tolist()} shared={cv['shared_lens'].tolist()}",
+          flush=True)
+    got = run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"],
+                      cv["max_group_seqs"], cv["max_shared_len"])
+    check(got, oracle_decode(q, seq_lens, bt, wl), "vs oracle")
+
+
+def test_cascade_decode_two_row_tiles_and_empty_private_part():
+    # 40 sequences of one agent at G = 4: 160 stacked rows, two row tiles; one
+    # sequence ends exactly where the shared prefix ends (no keys of its own),
+    # and an empty group sits between two others
+    invs = [Invocation(0, 1 + (i * 37) % 300) for i in range(40)] + [Invocation(1, 4)]
+    wl = build_workload("rows", 43, [777, 64], invs, num_q_heads=16, num_kv_heads=4,
+                        head_dim=128, num_blocks=2048)
+    q, seq_lens, bt, cv = grouped_batch(wl)
+    seq_lens = seq_lens.copy()
+    seq_lens[5] = 768                       # = the group's shared length
+    cu = [0, 40, 40, 41]
+    shared = [768, 0, 64]
+    print(f"[case] cascade rows: cu={cu} shared={shared}", flush=True)
+    got = run_cascade(wl, q, seq_lens, bt, cu, shared, 40, 768)
+    check(got, oracle_decode(q, seq_lens, bt, wl), "vs oracle")
+
+
+def test_cascade_decode_without_sharing_equals_paged_decode():
+    anchors, spec, hq, hkv, d = CASCADE_CASES["mixed_g4"]
+    invs = [Invocation(a, s, h) for a, s, h in spec]
+    wl = build_workload("noshare", 41, anchors, invs, num_q_heads=hq, num_kv_heads=hkv,
+                        head_dim=d, num_blocks=1024)
+    q, seq_lens = decode_view(wl)
+    got = run_cascade(wl, q, seq_lens, wl.block_tables, [0, wl.batch], [0], 1, 0)
+    ref = run_decode(wl)
+    # one group sharing nothing runs exactly the paged decode kernel's loop
+    assert np.array_equal(got, ref)
+
+
+def test_cascade_decode_batch_config():
+    wl = make_config("decode_batch")
+    q, seq_lens, bt, cv = grouped_batch(wl)
+    print(f"[case] cascade decode_batch groups={len(cv['shared_lens'])}", flush=True)
+    got = run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"],
+                      cv["max_group_seqs"], cv["max_shared_len"])
+    check(got, oracle_decode(q, seq_lens, bt, wl), "vs oracle")
+
+
+def test_cascade_workspace_reuse_and_debug_checks(monkeypatch):
+    from paper_2608_14624_amd import ops
+    anchors, spec, hq, hkv, d = CASCADE_CASES["mixed_g4"]
+    invs = [Invocation(a, s, h) for a, s, h in spec]
+    wl = build_workload("dbg", 41, anchors, invs, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                        num_blocks=1024)
+    q, seq_lens, bt, cv = grouped_batch(wl)
+    need = ops.cs_cascade_decode_workspace_bytes(wl.batch, hq, d, cv["max_shared_len"])
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")   # NaN-filled scratch
+    args = (wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"], cv["max_group_seqs"],
+            cv["max_shared_len"])
+    first = run_cascade(*args, workspace=ws)
+    second = run_cascade(*args, workspace=ws)
+    assert np.array_equal(first, second)
+    monkeypatch.setenv("CS_DEBUG_CHECK", "1")
+    assert np.array_equal(run_cascade(*args, workspace=ws), first)
+    bad = bt.copy()
+    g1 = int(cv["cu_groups"][0])
+    bad[g1 + 1, 0] = (bad[g1, 0] + 1) % wl.num_blocks     # breaks the sharing of block 0
+    with pytest.raises(ops.CacheScoutError, match="does not share"):
+        run_cascade(wl, q, seq_lens, bad, cv["cu_groups"], cv["shared_lens"],
+                    cv["max_group_seqs"], cv["max_shared_len"], workspace=ws)
+    with pytest.raises(ops.CacheScoutError, match="max_group_seqs"):
+        run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"], 1,
+                    cv["max_shared_len"], workspace=ws)
