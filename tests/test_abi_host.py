@@ -184,3 +184,44 @@ def test_decode_rejects_bad_arguments(kw, status):
 
 def test_decode_empty_batch_is_a_noop():
     assert ops.cs_paged_decode_attn_raw(**dict(DGOOD, batch=0, q=None)) == ops.CS_OK
+
+
+CGOOD = dict(DGOOD, cu_groups=FAKE, shared_lens=FAKE, num_groups=2, max_group_seqs=3,
+             max_shared_len=64, workspace=FAKE, workspace_bytes=1 << 20)
+
+
+def test_cascade_workspace_bytes():
+    # ceil(max_shared_len / 512) chunks x batch x Hq x (D + 2) floats
+    assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 0) == 0
+    assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 64) == 1 * 4 * 8 * 130 * 4
+    assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 513) == 2 * 4 * 8 * 130 * 4
+    assert ops.cs_cascade_decode_workspace_bytes(-1, 8, 128, 64) == -1
+    assert ops.cs_cascade_decode_workspace_bytes(4, 0, 128, 64) == -1
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(head_dim=96), ops.CS_ERR_UNSUPPORTED),
+    (dict(num_q_heads=64, num_kv_heads=2), ops.CS_ERR_UNSUPPORTED),
+    (dict(num_groups=0), ops.CS_ERR_INVALID_ARG),
+    (dict(num_groups=5), ops.CS_ERR_INVALID_ARG),           # more groups than sequences
+    (dict(max_group_seqs=0), ops.CS_ERR_INVALID_ARG),
+    (dict(max_group_seqs=5), ops.CS_ERR_INVALID_ARG),
+    (dict(max_shared_len=101), ops.CS_ERR_INVALID_ARG),     # beyond max_seq_len
+    (dict(max_shared_len=-16), ops.CS_ERR_INVALID_ARG),
+    (dict(cu_groups=None), ops.CS_ERR_INVALID_ARG),
+    (dict(shared_lens=None), ops.CS_ERR_INVALID_ARG),
+    (dict(workspace=None), ops.CS_ERR_INVALID_ARG),
+    (dict(workspace=FAKE + 8), ops.CS_ERR_INVALID_ARG),
+    (dict(workspace_bytes=100), ops.CS_ERR_INVALID_ARG),
+    (dict(workspace_bytes=-1), ops.CS_ERR_INVALID_ARG),
+])
+def test_cascade_rejects_bad_arguments(kw, status):
+    args = dict(CGOOD)
+    args.update(kw)
+    assert ops.cs_cascade_decode_attn_raw(**args) == status
+
+
+def test_cascade_empty_batch_is_a_noop():
+    assert ops.cs_cascade_decode_attn_raw(**dict(CGOOD, batch=0, q=None, num_groups=0,
+                                                 workspace=None)) == ops.CS_OK
