@@ -209,7 +209,8 @@ def bench_copy(args, dev):
             ops.cs_kv_offload(ids, k_pool, v_pool, host_k, host_v, stream=stream)
         peak, bound, unit_desc = PEAK_PCIE5_X16_GBS, "host_link", f"{n} blocks"
     kernel, sources = {
-        "decode": ("paged_decode_attn_kernel", ("paper_2608_14624_amd/csrc/paged_decode_attn.hip",)),
+        "decode": ("paged_decode_attn_kernel<128, false>",
+                   ("paper_2608_14624_amd/csrc/paged_decode_attn.hip",)),
         "cascade_decode": ("prefill_paged_attn_kernel<128, true> + paged_decode_attn_kernel<128, true>",
                            ("paper_2608_14624_amd/csrc/prefill_paged_attn.hip",
                             "paper_2608_14624_amd/csrc/paged_decode_attn.hip")),
@@ -447,7 +448,7 @@ def main():
                                  "frac_link": round(iso_gbs / PEAK_PCIE5_X16_GBS, 4),
                                  "avg_launch_us": round(iso * 1e3, 2)}}
     khash = source_hash(KERNEL_SOURCES[:1])
-    traffic = load_traffic("prefill_paged_attn_kernel<128>", args.workload, khash)
+    traffic = load_traffic("prefill_paged_attn_kernel<128, false>", args.workload, khash)
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -469,7 +470,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
-                     "kernel": "prefill_paged_attn_kernel<128>",
+                     "kernel": "prefill_paged_attn_kernel<128, false>",
                      "avg_launch_us": round(attn_avg_ms * 1e3, 2),
                      "flop_per_launch": step_flops // n_launch},
         "prefetch": prefetch,
