@@ -32,6 +32,15 @@
 // each serve one KV head and its K/V stays in that XCD's L2; token tiles are
 // issued from the last (most keys) to the first.
 //
+// Ping-pong kernel (launches with at least one work-group per CU): 8 waves,
+// 256 query rows per work-group, one work-group per CU, and the two waves of
+// a SIMD are offset by half a step: waves 0-3 run an iteration as [MFMAs:
+// PV of the previous step + QK^T of this one][softmax of this step], waves
+// 4-7 as [softmax of the previous step][the same MFMAs], so one wave's
+// matrix work overlaps the other's vector work between two barriers.  The
+// K/V tiles serve 8 waves instead of 4 (waves 0-3 stage K, 4-7 stage V), and
+// each row's arithmetic is the same as in the four-wave kernel, bit for bit.
+//
 // Stacked mode (the shared-prefix half of cascade attention): the query rows
 // of a work-group are any 128 (sequence, query head) pairs of one group of
 // sequences that share a prefix and one KV head; they attend, without a
@@ -42,6 +51,8 @@
 #include "internal.h"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace cs {
 namespace {
@@ -58,6 +69,11 @@ constexpr int kBN = 64;       // keys per step
 constexpr int kNQ = 32;       // query rows per wave
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kPPWaves = 8;             // ping-pong kernel: two groups of four waves
+constexpr int kPPThreads = 64 * kPPWaves;
+// the ping-pong kernel takes a launch that has at least one work-group per CU
+// (MI355X: 256 CUs); smaller launches keep two four-wave work-groups per CU
+constexpr long long kPPMinGrid = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct Params {
@@ -462,16 +478,302 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Params p) {
+  __shared__ Lds<D> sm;
+  constexpr int kStride = Lds<D>::kStride;
+  constexpr int vStride = Lds<D>::vStride;
+  constexpr int KS = D / 16;     // MFMA k-steps over the head dim
+  constexpr int DT = D / 32;     // 32-wide output tiles over the head dim
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int qi = lane & 31;
+  const int half = lane >> 5;
+  // group A (waves 0-3) runs MFMA-first, group B (waves 4-7) VALU-first; the
+  // two waves of a SIMD belong to different groups
+  const bool group_b = __builtin_amdgcn_readfirstlane(wave) >= 4;
+
+  // ---- work tile (same order as the four-wave kernel) -----------------
+  const int wg = blockIdx.x;
+  const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
+  const int g = wg % p.num_kv_heads;
+  const int sub = wg / p.num_kv_heads;
+  const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
+  const int rest = sub / tiles_per_kv;
+  const int r = rest % p.batch;
+  const int token_tile = p.token_tiles - 1 - rest / p.batch;
+  const int q0 = p.cu_q_lens[r];
+  const int S = p.cu_q_lens[r + 1] - q0;
+  const int t0 = token_tile * p.span;
+  if (t0 >= S) return;
+  const int P = p.prefix_lens[r];
+  const int L = P + S;
+  const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
+  const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
+  const bool row_valid = t < S;
+  const size_t qrow = ((size_t)(q0 + (row_valid ? t : 0)) * p.num_q_heads + h) * D;
+  const int qpos = row_valid ? P + t : L - 1;               // last visible key
+  const int kv_end = P + min(S, t0 + p.span);               // keys the tile needs
+  const int n_steps = (kv_end + kBN - 1) / kBN;
+  const int n_blk = (L + kBlock - 1) / kBlock;
+  const int32_t* bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
+  // first key position some row of this wave cannot see
+  const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
+  const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
+  const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
+
+  // ---- Q^T operand: lane holds query qi, dims ks*16 + half*8 .. +7 -----
+  bf16x8 qreg[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (row_valid) v = *reinterpret_cast<const uint4*>(p.q + qrow + ks * 16 + half * 8);
+    qreg[ks] = as_bf16x8(v);
+  }
+
+  // ---- staging: waves 0-3 move K, waves 4-7 move V; wave w moves pool block
+  // 4*step + (w & 3).  K is staged for the step the next iteration's logits
+  // use, V for the step whose probabilities the next iteration multiplies.
+  constexpr int kChunksPerRow = D / 8;
+  constexpr int kKLoads = kBlock * kChunksPerRow / 64;             // 4 (D=128), 2 (D=64)
+  const int slot_u = __builtin_amdgcn_readfirstlane(wave & 3);
+  const uint16_t* my_base = (group_b ? p.v_pool : p.k_pool) + (size_t)g * tile_elems;
+  const __attribute__((address_space(4))) int32_t* bt_c =
+      (const __attribute__((address_space(4))) int32_t*)bt;
+  auto block_id = [&](int step) __attribute__((always_inline)) -> int {
+    const int lb = step * (kBN / kBlock) + slot_u;
+    return (step < n_steps && lb < n_blk) ? bt_c[lb] : -1;          // -1: past the end
+  };
+  using Stage = uint4[kKLoads];
+  uint4 stage[2][kKLoads];
+  auto load_tile = [&](Stage& dst, int id) __attribute__((always_inline)) {
+    if (id >= 0) {
+      const uint16_t* src = my_base + (size_t)id * slot_elems;
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) {
+        const int c = lane + 64 * u;
+        dst[u] = *reinterpret_cast<const uint4*>(src + (c / kChunksPerRow) * D + (c % kChunksPerRow) * 8);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) dst[u] = make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_tile = [&](const Stage& src, uint16_t* dst, int stride) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < kKLoads; ++u) {
+      const int c = lane + 64 * u;
+      const int key = slot_u * kBlock + c / kChunksPerRow;
+      *reinterpret_cast<uint4*>(&dst[key * stride + (c % kChunksPerRow) * 8]) = src[u];
+    }
+  };
+  // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
+  // transposing reads (ds_read_b64_tr_b16: lane j of a 16-lane group gets
+  // M[4e + j/4][j%4] of the 8-byte rows its lanes address).
+  const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  auto v_frag = [&](const uint16_t* vbuf, int ks2, int dt) __attribute__((always_inline)) -> bf16x8 {
+    const uint16_t* base = &vbuf[(16 * ks2 + tr_row) * vStride + 32 * dt + tr_col];
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 8 * vStride));
+    const i16x4 lohi[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8, lohi);
+  };
+
+  auto run = [&](auto group_tag) __attribute__((always_inline)) {
+    constexpr bool kB = decltype(group_tag)::value;
+    f32x16 oacc[DT];
+  #pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+    f32x16 s_acc[2];             // logits of the step whose softmax is pending
+    bf16x8 pb[kBN / 16];         // probabilities of the step whose PV is pending
+    float m_run = -INFINITY;     // running max of the raw (unscaled) logits
+    float l_part[4] = {0.f, 0.f, 0.f, 0.f};
+    const float c = p.scale_log2;
+
+    // M phase of iteration j: O += P_{j-1} V_{j-1}, then S_j = K_j Q^T
+    auto mfma_phase = [&](int j) __attribute__((always_inline)) {
+      __builtin_amdgcn_s_setprio(1);
+      if (j >= 1) {
+        const uint16_t* vbuf = sm.v[(j - 1) & 1];
+  #pragma unroll
+        for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
+  #pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), pb[ks2], oacc[dt], 0, 0, 0);
+        }
+        // interleave, the reads one 16-key slice ahead of their MFMAs
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
+#pragma unroll
+        for (int ks2 = 1; ks2 < kBN / 16; ++ks2) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (j < n_steps) {
+        const uint16_t* kbuf = sm.k[j & 1];
+        s_acc[0] = f32x16{};
+        s_acc[1] = f32x16{};
+  #pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+  #pragma unroll
+          for (int mt = 0; mt < 2; ++mt) {
+            const uint4 a = *reinterpret_cast<const uint4*>(&kbuf[(mt * 32 + qi) * kStride + ks * 16 + half * 8]);
+            s_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], s_acc[mt], 0, 0, 0);
+          }
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+#pragma unroll
+        for (int ks = 2; ks < KS; ++ks) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
+      }
+      __builtin_amdgcn_s_setprio(0);
+    };
+
+    // V phase for step x: mask, online softmax, P_x in bf16, row sums
+    auto valu_phase = [&](int x) __attribute__((always_inline)) {
+      if (x < 0 || x >= n_steps) return;
+      const int kstart = x * kBN;
+      // accumulator register rr of tile mt holds key
+      //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
+      if (kstart + kBN - 1 > wave_qmin) {
+  #pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+  #pragma unroll
+          for (int rr = 0; rr < 16; ++rr) {
+            const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
+            s_acc[mt][rr] = (kj <= qpos) ? s_acc[mt][rr] : -INFINITY;
+          }
+        }
+      }
+      float mloc = -INFINITY;
+  #pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+  #pragma unroll
+        for (int rr = 0; rr < 16; ++rr) mloc = fmaxf(mloc, s_acc[mt][rr]);
+      }
+      mloc = pair_max(mloc);
+      // lazy rescale: move the reference max only when a row's max grew by
+      // more than 2^8 in probability (true for every row at the first step)
+      const bool grow = (mloc - m_run) * c > 8.f;
+      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+        const float m_new = grow ? mloc : m_run;
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+        m_run = m_new;
+  #pragma unroll
+        for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
+  #pragma unroll
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+      }
+      const float mc = m_run * c;
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  #pragma unroll
+      for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
+        const int mt = ks2 >> 1;
+        const int rb = (ks2 & 1) * 8;
+  #pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2)
+          pb[ks2][s2] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s_acc[mt][rb + s2], c, -mc));
+        // row sum over the same bf16 probabilities the PV product uses
+        l_part[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 0, 1), ones, l_part[0], false);
+        l_part[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 2, 3), ones, l_part[1], false);
+        l_part[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 4, 5), ones, l_part[2], false);
+        l_part[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 6, 7), ones, l_part[3], false);
+      }
+    };
+
+    // ---- prologue ------------------------------------------------------
+    // K waves: K_0 into LDS, K_1 and K_2 in registers; V waves: V_0 and V_1
+    // in registers (V_j is stored at iteration j, K_{j+1} at iteration j).
+    if (!kB) {
+      load_tile(stage[0], block_id(0));
+      store_tile(stage[0], sm.k[0], kStride);
+      load_tile(stage[1], block_id(1));
+      load_tile(stage[0], block_id(2));
+    } else {
+      load_tile(stage[0], block_id(0));
+      load_tile(stage[1], block_id(1));
+    }
+
+    // One iteration: stage data for the next iteration, then the two phases in
+    // group order.  Iteration j reads K_j and V_{j-1}; it stores K_{j+1} into
+    // the K buffer K_{j-1} used and V_j into the V buffer V_{j-2} used, both
+    // read in iteration j-1, before this iteration's barrier.
+    auto iteration = [&](const int j, Stage& st) __attribute__((always_inline)) {
+      __syncthreads();
+      if (!kB) {
+        if (j + 1 < n_steps) store_tile(st, sm.k[(j + 1) & 1], kStride);
+        if (j + 3 < n_steps) load_tile(st, block_id(j + 3));
+      } else {
+        if (j < n_steps) store_tile(st, sm.v[j & 1], vStride);
+        if (j + 2 < n_steps) load_tile(st, block_id(j + 2));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (!kB) {
+        mfma_phase(j);
+        __builtin_amdgcn_sched_barrier(0);
+        valu_phase(j);
+      } else {
+        valu_phase(j - 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_phase(j);
+      }
+    };
+    // register stage of iteration j: K waves stage[(j+1)&1] (K_{j+1} is
+    // stored, K_{j+3} loaded), V waves stage[j&1] (V_j stored, V_{j+2} loaded);
+    // unrolled by two so the stage is a constant
+    for (int j = 0; j <= n_steps; j += 2) {
+      if (!kB) {
+        iteration(j, stage[1]);
+        if (j + 1 <= n_steps) iteration(j + 1, stage[0]);
+      } else {
+        iteration(j, stage[0]);
+        if (j + 1 <= n_steps) iteration(j + 1, stage[1]);
+      }
+    }
+    const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
+    const float l_tot = pair_sum(l_run);
+    const float inv = 1.f / l_tot;
+    if (row_valid) {
+      uint16_t* orow = p.out + qrow;
+  #pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+  #pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          bf16x4 o;
+  #pragma unroll
+          for (int u = 0; u < 4; ++u) o[u] = (__bf16)(oacc[dt][rg * 4 + u] * inv);
+          *reinterpret_cast<uint2*>(orow + dt * 32 + 8 * rg + 4 * half) = __builtin_bit_cast(uint2, o);
+        }
+      }
+    }
+
+  };
+  if (group_b) run(std::true_type{});
+  else run(std::false_type{});
+}
+
 }  // namespace
 
 AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads) {
   AttnGeometry geo;
   const int group = num_q_heads / num_kv_heads;
   geo.heads_per_wg = (group % 4 == 0) ? 4 : (group % 2 == 0) ? 2 : 1;
-  geo.span = kNQ * (kWaves / geo.heads_per_wg);
-  geo.token_tiles = (max_q_len + geo.span - 1) / geo.span;
   geo.head_tiles = num_q_heads / geo.heads_per_wg;
-  geo.grid = (long long)geo.token_tiles * batch * geo.head_tiles;
+  for (const int waves : {kPPWaves, kWaves}) {
+    geo.waves = waves;
+    geo.span = kNQ * (waves / geo.heads_per_wg);
+    geo.token_tiles = (max_q_len + geo.span - 1) / geo.span;
+    geo.grid = (long long)geo.token_tiles * batch * geo.head_tiles;
+    if (waves == kPPWaves && geo.grid >= kPPMinGrid) break;
+  }
   return geo;
 }
 
@@ -495,11 +797,17 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
   p.token_tiles = geo.token_tiles;
   p.head_tiles = geo.head_tiles;
   p.scale_log2 = a.scale * kLog2e;
-  const dim3 grid((unsigned)geo.grid), block(kThreads);
-  if (a.head_dim == 128) {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, false>), grid, block, 0, stream, p);
+  const dim3 grid((unsigned)geo.grid);
+  if (geo.waves == kPPWaves) {
+    if (a.head_dim == 128) {
+      hipLaunchKernelGGL(prefill_paged_attn_pp_kernel<128>, grid, dim3(kPPThreads), 0, stream, p);
+    } else {
+      hipLaunchKernelGGL(prefill_paged_attn_pp_kernel<64>, grid, dim3(kPPThreads), 0, stream, p);
+    }
+  } else if (a.head_dim == 128) {
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, false>), grid, dim3(kThreads), 0, stream, p);
   } else {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, false>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, false>), grid, dim3(kThreads), 0, stream, p);
   }
   return hipGetLastError();
 }

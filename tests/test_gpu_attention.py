@@ -198,6 +198,34 @@ def test_run_to_run_determinism(P):
         assert torch.equal(a.view(torch.int16), dw.out.view(torch.int16))
 
 
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 8, 64), (12, 4, 128), (8, 8, 128)])
+def test_wide_and_four_wave_kernels_agree_bitwise(P, hq, hkv, d):
+    """A batch large enough for the 8-wave ping-pong kernel, and its first
+    invocation alone (a launch below one work-group per CU, which takes the
+    four-wave kernel), give bit-identical rows: each row's arithmetic is the
+    same in both."""
+    _, pipeline = P
+    invs = [Invocation(i % 3, 300 + 37 * i) for i in range(16)]
+    wl = build_workload("wide", 12, [520, 77, 1200], invs, num_q_heads=hq, num_kv_heads=hkv,
+                        head_dim=d, num_blocks=4096)
+    print(f"[case] wide vs four-wave hq={hq} hkv={hkv} d={d} total_q={wl.total_q}", flush=True)
+    dw = pipeline.DeviceWorkload(wl)
+    dw.attention()
+    first = pipeline.SubBatch(dw, 0, 1)
+    alone = torch.full_like(first.out, float("nan"))
+    from paper_2608_14624_amd import ops
+    ops.cs_prefill_paged_attn(first.q, dw.k_pool, dw.v_pool, first.block_tables,
+                              first.prefix_lens, first.cu_q_lens, alone,
+                              max_q_len=first.max_q_len, max_kv_len=first.max_kv_len,
+                              scale=wl.scale)
+    torch.cuda.synchronize()
+    assert torch.equal(alone.view(torch.int16), first.out.view(torch.int16))
+    samples = sample_rows(wl, 200, seed=5)
+    mx, mean = compare_rows(wl, dw.out_bits(), samples)
+    print(f"    {len(samples)} rows: max_abs={mx:.3e} mean_abs={mean:.3e}", flush=True)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
 def test_hit_rows_match_miss_rows(P):
     # the same prompt served as a hit and as a miss
     for prefix, suffix in ((256, 64), (37, 100), (1000, 1)):
