@@ -57,10 +57,11 @@ def build(verbose=False):
         objects = []
         for src in host_sources:
             obj = os.path.join(work, os.path.basename(src) + ".o")
-            run([cxx(), "-O2", "-std=c++17", "-fPIC", "-ffp-contract=off",
+            run([cxx(), "-O2", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-ffp-contract=off",
                  "-Wall", "-Wextra", *includes, "-c", src, "-o", obj], verbose)
             objects.append(obj)
         run([hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+             "-fvisibility=hidden",
              # keep the compiler from forming packed fp32 ops
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              # MFMA accumulators in arch VGPRs: the softmax rescale then works on

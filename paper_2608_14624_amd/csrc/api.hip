@@ -246,6 +246,8 @@ int validate_decode(const void* q, const void* k_pool, const void* v_pool,
 
 }  // namespace
 
+// the C ABI is the only thing the library exports (built with -fvisibility=hidden)
+#pragma GCC visibility push(default)
 extern "C" {
 
 const char* cs_status_string(int status) {
@@ -548,3 +550,4 @@ int cs_kv_offload(const int32_t* src_block_ids, int32_t n, const void* k_pool, c
 }
 
 }  // extern "C"
+#pragma GCC visibility pop

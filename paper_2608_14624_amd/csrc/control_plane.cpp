@@ -98,6 +98,8 @@ void refresh_row_entropy(cs_scout* s, int32_t i) {
 
 }  // namespace
 
+// the C ABI is the only thing the library exports (built with -fvisibility=hidden)
+#pragma GCC visibility push(default)
 extern "C" {
 
 void cs_scout_default_params(cs_scout_params* out) {
@@ -297,3 +299,4 @@ int64_t cs_scout_state_bytes(const cs_scout* s) {
 }
 
 }  // extern "C"
+#pragma GCC visibility pop

@@ -256,13 +256,12 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     return lb < n_blk ? bt_c[lb] : -1;                               // -1: past the end
   };
 
-  // K runs one step ahead of V: iteration j reads K_{j+1} (for the next
-  // step's logits) and V_j (for this step's PV product) and writes K_{j+2}
-  // and V_{j+1} into the other halves of the two double buffers, so one
-  // barrier per step separates every write from the reads it must follow.
-  // Two register stages: the loads of step j+3 are issued at iteration j
-  // into the stage whose data (step j+1) was just stored, so every global
-  // load has two steps to arrive.
+  // Iteration j reads K_j and V_j from buffer j&1 and, after the barrier
+  // that ends iteration j-1's reads of buffer (j+1)&1, writes K_{j+1} and
+  // V_{j+1} there, so one barrier per step separates every write from the
+  // reads it must follow.  Two register stages: the loads of step j+3 are
+  // issued at iteration j into the stage whose data (step j+1) was just
+  // stored, so every global load has two steps to arrive.
   using Stage = uint4[kKLoads];
   uint4 kreg[2][kKLoads];
   uint4 vreg[2][kKLoads];

@@ -225,3 +225,16 @@ def test_cascade_rejects_bad_arguments(kw, status):
 def test_cascade_empty_batch_is_a_noop():
     assert ops.cs_cascade_decode_attn_raw(**dict(CGOOD, batch=0, q=None, num_groups=0,
                                                  workspace=None)) == ops.CS_OK
+
+
+def test_library_exports_only_the_declared_calls():
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--defined-only", ops.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    text_symbols = sorted(line.split()[-1] for line in out.splitlines()
+                          if len(line.split()) == 3 and line.split()[1] == "T")
+    assert text_symbols == declared_functions()
