@@ -76,6 +76,19 @@ def load_traffic(kernel, workload, kernel_hash):
     return entry.get("bytes_per_launch")
 
 
+def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim):
+    """Which attention kernel a launch runs: the 8-wave ping-pong kernel when
+    its grid has at least one work-group per CU (256), else the four-wave one
+    (the library's launch rule, repeated here only to label the result)."""
+    group = num_q_heads // num_kv_heads
+    hw = 4 if group % 4 == 0 else 2 if group % 2 == 0 else 1
+    span = 32 * (8 // hw)
+    grid = -(-max_q_len // span) * batch * (num_q_heads // hw)
+    if grid >= 256:
+        return f"prefill_paged_attn_pp_kernel<{head_dim}>"
+    return f"prefill_paged_attn_kernel<{head_dim}, false>"
+
+
 def cpu_baseline(wl, budget_s=20.0):
     """The float64 oracle on whole invocations of the same workload, as many as
     fit the time budget (at least one), in TFLOP/s of algorithmic work."""
@@ -333,6 +346,10 @@ def main():
     ap.add_argument("--workload", default="llama70b_prefetch",
                     choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--policy", default="order", choices=("order", "scout"),
+                    help="prefetch target: the next agent in dispatch order (default) or the "
+                         "control plane's between-step decision (cs_scout_*); the warmup "
+                         "steps let it learn the dispatch cycle")
     ap.add_argument("--component", default="pipeline",
                     choices=("pipeline", "kv_write", "kv_offload", "decode", "cascade_decode",
                              "control_plane"),
@@ -380,7 +397,10 @@ def main():
     main_stream = torch.cuda.current_stream(dev)
     if wl.prefetch_dst is not None:
         # serving order with the next agent's prefetch overlapped on a side stream
-        pipe = pipeline.AgentPipeline(dw)
+        policy = None
+        if args.policy == "scout":
+            policy = pipeline.ScoutPolicy(wl, sorted({inv.agent for inv in wl.invocations}))
+        pipe = pipeline.AgentPipeline(dw, policy=policy)
         pipe.stage_first()
         n_launch = len(pipe.agents)
         step_flops, step_bytes, warm = pipe.flops, pipe.prefetch_bytes, pipe.step
@@ -409,6 +429,7 @@ def main():
         pipe.step(timing=list(zip(p_ev[si], a_ev[si])))
 
     torch.cuda.synchronize()
+    hits0, misses0 = (pipe.hits, pipe.misses) if pipe is not None else (0, 0)
     t0 = time.perf_counter()
     for si in range(args.steps):
         timed_step(si)
@@ -448,7 +469,15 @@ def main():
                                  "frac_link": round(iso_gbs / PEAK_PCIE5_X16_GBS, 4),
                                  "avg_launch_us": round(iso * 1e3, 2)}}
     khash = source_hash(KERNEL_SOURCES[:1])
-    traffic = load_traffic("prefill_paged_attn_kernel<128, false>", args.workload, khash)
+    if pipe is not None:
+        kernel_names = sorted({attention_kernel_name(b.hi - b.lo, b.max_q_len, wl.num_q_heads,
+                                                     wl.num_kv_heads, wl.head_dim)
+                               for b in pipe.batches})
+    else:
+        kernel_names = [attention_kernel_name(wl.batch, wl.max_q_len, wl.num_q_heads,
+                                              wl.num_kv_heads, wl.head_dim)]
+    kernel_name = " + ".join(kernel_names)
+    traffic = load_traffic(kernel_name, args.workload, khash)
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -470,10 +499,12 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
-                     "kernel": "prefill_paged_attn_kernel<128, false>",
+                     "kernel": kernel_name,
                      "avg_launch_us": round(attn_avg_ms * 1e3, 2),
                      "flop_per_launch": step_flops // n_launch},
         "prefetch": prefetch,
+        "prefetch_policy": None if pipe is None else {
+            "name": args.policy, "hits": pipe.hits - hits0, "misses": pipe.misses - misses0},
         "kernel_sha": khash,
         "cpu_baseline": None,
     }

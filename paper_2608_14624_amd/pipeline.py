@@ -241,6 +241,10 @@ class AgentPipeline:
                     if p1 is not None:
                         p1.record(self.side)
                     self.events[target].record(self.side)
+            elif p0 is not None:
+                # no prefetch this turn: an empty interval keeps the events recorded
+                p0.record(self.side)
+                p1.record(self.side)
             if a0 is not None:
                 a0.record(main)
             self.batches[k].attention(stream=main)
