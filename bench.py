@@ -181,14 +181,16 @@ def bench_copy(args, dev):
             cu = torch.from_numpy(cv["cu_groups"]).to(dev)
             shared = torch.from_numpy(cv["shared_lens"]).to(dev)
             need = ops.cs_cascade_decode_workspace_bytes(wl.batch, wl.num_q_heads, d,
-                                                         cv["max_shared_len"])
+                                                         cv["max_shared_len"],
+                                                         cv["max_rest_len"])
             ws = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
 
             def fn():
                 ops.cs_cascade_decode_attn(q, k_pool, v_pool, bt, seq_lens, cu, shared, out,
                                            max_seq_len=max_len,
                                            max_group_seqs=cv["max_group_seqs"],
-                                           max_shared_len=cv["max_shared_len"], scale=wl.scale,
+                                           max_shared_len=cv["max_shared_len"],
+                                           max_rest_len=cv["max_rest_len"], scale=wl.scale,
                                            workspace=ws, stream=stream)
         peak, bound = PEAK_HBM_GBS, "hbm"
         unit_desc = (f"{wl.batch} sequences in {len(cv['shared_lens'])} agent groups, "
@@ -224,7 +226,8 @@ def bench_copy(args, dev):
     kernel, sources = {
         "decode": ("paged_decode_attn_kernel<128, false>",
                    ("paper_2608_14624_amd/csrc/paged_decode_attn.hip",)),
-        "cascade_decode": ("prefill_paged_attn_kernel<128, true> + paged_decode_attn_kernel<128, true>",
+        "cascade_decode": ("prefill_paged_attn_kernel<128, true> + paged_decode_attn_kernel<128, true>"
+                           " + cascade_merge_kernel<128>",
                            ("paper_2608_14624_amd/csrc/prefill_paged_attn.hip",
                             "paper_2608_14624_amd/csrc/paged_decode_attn.hip")),
         "kv_write": ("kv_write_kernel", ("paper_2608_14624_amd/csrc/kv_copy.hip",)),

@@ -204,9 +204,11 @@ int cs_paged_decode_attn(const void *q, const void *k_pool, const void *v_pool,
  * head the queries of all its sequences (and of the query heads of that KV
  * head) are stacked and attend once over the shared keys, in chunks of 512
  * keys; each chunk leaves a partial result (O relative to its running max m,
- * m and the sum l) in the workspace.  Each sequence then attends its own keys
- * shared_lens[g] .. seq_lens[r]-1 and merges all partials with log-sum-exp
- * weights.  The output equals cs_paged_decode_attn's up to rounding order.
+ * m and the sum l) in the workspace.  Each sequence's own keys
+ * shared_lens[g] .. seq_lens[r]-1 are attended in segments of 1024 keys,
+ * each leaving a partial too, and a last launch merges all partials of a
+ * row with log-sum-exp weights.  The output equals cs_paged_decode_attn's up
+ * to rounding order.
  *
  * Arguments (those of cs_paged_decode_attn, plus)
  *   cu_groups       device, int32 [num_groups + 1]: 0 = cu_groups[0] <= ...
@@ -220,11 +222,15 @@ int cs_paged_decode_attn(const void *q, const void *k_pool, const void *v_pool,
  *                   larger).
  *   max_shared_len  host bound on shared_lens, <= max_seq_len; sizes the launch
  *                   and the workspace.
+ *   max_rest_len    host bound on every sequence's own keys,
+ *                   seq_lens[r] - shared_lens[g] <= max_rest_len <= max_seq_len.
+ *                   ceil(max_shared_len / 512) + ceil(max_rest_len / 1024)
+ *                   above 512 is CS_ERR_UNSUPPORTED.
  *   workspace       device, 16-byte aligned, caller-owned scratch of at least
  *                   cs_cascade_decode_workspace_bytes(batch, num_q_heads,
- *                   head_dim, max_shared_len) bytes (may be NULL when that is
- *                   0); its contents are undefined after the call.  Calls that
- *                   share a workspace must be ordered on one stream.
+ *                   head_dim, max_shared_len, max_rest_len) bytes; its contents
+ *                   are undefined after the call.  Calls that share a
+ *                   workspace must be ordered on one stream.
  * With CS_DEBUG_CHECK=1 the group structure, the shared block ids and the
  * decode metadata are validated on the host first.
  */
@@ -233,15 +239,16 @@ int cs_cascade_decode_attn(const void *q, const void *k_pool, const void *v_pool
                            int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
                            const int32_t *cu_groups, const int32_t *shared_lens,
                            int32_t num_groups, int32_t max_group_seqs, int32_t max_shared_len,
-                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                           int32_t block_size, float scale, void *workspace,
+                           int32_t max_rest_len, int32_t num_q_heads, int32_t num_kv_heads,
+                           int32_t head_dim, int32_t block_size, float scale, void *workspace,
                            int64_t workspace_bytes, void *out, cs_stream_t stream);
 
 /* Workspace bytes cs_cascade_decode_attn needs:
- * ceil(max_shared_len / 512) * batch * num_q_heads * (head_dim + 2) * 4;
- * -1 for a negative or zero size argument. */
+ * (ceil(max_shared_len / 512) + ceil(max_rest_len / 1024)) * batch *
+ * num_q_heads * (head_dim + 2) * 4; -1 for a negative size or a zero head
+ * count or head_dim. */
 int64_t cs_cascade_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t head_dim,
-                                          int32_t max_shared_len);
+                                          int32_t max_shared_len, int32_t max_rest_len);
 
 /*
  * KV write-back: store the K/V rows of new tokens into their pool slots.

@@ -154,7 +154,7 @@ int debug_check_decode(const int32_t* block_tables, const int32_t* seq_lens, int
 // that every sequence of the group holds, through identical block ids.
 int debug_check_groups(const int32_t* block_tables, const int32_t* seq_lens,
                        const int32_t* cu_groups, const int32_t* shared_lens, int batch,
-                       int num_groups, int max_group_seqs, int max_shared_len,
+                       int num_groups, int max_group_seqs, int max_shared_len, int max_rest_len,
                        int max_blocks_per_seq, hipStream_t stream) {
   std::vector<int32_t> sl, bt, cu, sh;
   hipError_t e = copy_to_host(sl, seq_lens, (size_t)batch, stream);
@@ -175,6 +175,9 @@ int debug_check_groups(const int32_t* block_tables, const int32_t* seq_lens,
     for (int r = cu[g]; r < cu[g + 1]; ++r) {
       if (sh[g] > sl[r])
         return fail(CS_ERR_INVALID_ARG, "shared_lens[%d] = %d exceeds seq_lens[%d] = %d", g, sh[g], r, sl[r]);
+      if (sl[r] - sh[g] > max_rest_len)
+        return fail(CS_ERR_INVALID_ARG, "sequence %d has %d own keys (max_rest_len %d)", r,
+                    sl[r] - sh[g], max_rest_len);
       for (int b = 0; b < sh[g] / 16; ++b) {
         if (bt[(size_t)r * max_blocks_per_seq + b] != bt[(size_t)cu[g] * max_blocks_per_seq + b])
           return fail(CS_ERR_INVALID_ARG, "sequence %d does not share block %d of group %d", r, b, g);
@@ -397,11 +400,13 @@ int cs_paged_decode_attn(const void* q, const void* k_pool, const void* v_pool,
 }
 
 int64_t cs_cascade_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t head_dim,
-                                           int32_t max_shared_len) {
-  if (batch < 0 || num_q_heads <= 0 || head_dim <= 0 || max_shared_len < 0) return -1;
+                                           int32_t max_shared_len, int32_t max_rest_len) {
+  if (batch < 0 || num_q_heads <= 0 || head_dim <= 0 || max_shared_len < 0 || max_rest_len < 0)
+    return -1;
   const long long chunk = (long long)cs::kCascadeChunkSteps * 64;
-  const long long chunks = (max_shared_len + chunk - 1) / chunk;
-  return (int64_t)(chunks * batch * num_q_heads * (head_dim + 2) * (long long)sizeof(float));
+  const long long parts = (max_shared_len + chunk - 1) / chunk +
+                          (max_rest_len + cs::kCascadeSegmentKeys - 1) / cs::kCascadeSegmentKeys;
+  return (int64_t)(parts * batch * num_q_heads * (head_dim + 2) * (long long)sizeof(float));
 }
 
 int cs_cascade_decode_attn(const void* q, const void* k_pool, const void* v_pool,
@@ -409,15 +414,16 @@ int cs_cascade_decode_attn(const void* q, const void* k_pool, const void* v_pool
                            int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
                            const int32_t* cu_groups, const int32_t* shared_lens,
                            int32_t num_groups, int32_t max_group_seqs, int32_t max_shared_len,
-                           int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                           int32_t block_size, float scale, void* workspace,
+                           int32_t max_rest_len, int32_t num_q_heads, int32_t num_kv_heads,
+                           int32_t head_dim, int32_t block_size, float scale, void* workspace,
                            int64_t workspace_bytes, void* out, cs_stream_t stream) {
   bool noop;
   int st0 = validate_decode(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
                             max_blocks_per_seq, num_blocks, num_q_heads, num_kv_heads, head_dim,
                             block_size, scale, out, &noop);
   if (st0 != CS_OK) return st0;
-  if (num_groups < 0 || max_group_seqs < 0 || max_shared_len < 0 || workspace_bytes < 0)
+  if (num_groups < 0 || max_group_seqs < 0 || max_shared_len < 0 || max_rest_len < 0 ||
+      workspace_bytes < 0)
     return fail(CS_ERR_INVALID_ARG, "negative size argument");
   if (noop) return ok();
   if (num_groups < 1 || num_groups > batch)
@@ -426,8 +432,11 @@ int cs_cascade_decode_attn(const void* q, const void* k_pool, const void* v_pool
     return fail(CS_ERR_INVALID_ARG, "max_group_seqs %d outside [1, batch = %d]", max_group_seqs, batch);
   if (max_shared_len > max_seq_len)
     return fail(CS_ERR_INVALID_ARG, "max_shared_len %d exceeds max_seq_len %d", max_shared_len, max_seq_len);
+  if (max_rest_len > max_seq_len)
+    return fail(CS_ERR_INVALID_ARG, "max_rest_len %d exceeds max_seq_len %d", max_rest_len, max_seq_len);
   if (!cu_groups || !shared_lens) return fail(CS_ERR_INVALID_ARG, "null pointer argument");
-  const int64_t need = cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim, max_shared_len);
+  const int64_t need = cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim, max_shared_len,
+                                                         max_rest_len);
   if (need > 0) {
     if (!workspace || !aligned16(workspace))
       return fail(CS_ERR_INVALID_ARG, "workspace must be a 16-byte aligned device buffer");
@@ -436,15 +445,19 @@ int cs_cascade_decode_attn(const void* q, const void* k_pool, const void* v_pool
                   (long long)need);
   }
   const cs::CascadeGeometry geo = cs::cascade_geometry(num_groups, max_group_seqs, max_shared_len,
-                                                       num_q_heads, num_kv_heads);
-  if (geo.grid > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
+                                                       max_rest_len, num_q_heads, num_kv_heads);
+  if (geo.grid > 0x7fffffffLL || (long long)batch * num_kv_heads * geo.segments > 0x7fffffffLL)
+    return fail(CS_ERR_INVALID_ARG, "launch too large");
+  if (geo.chunks + geo.segments > cs::kCascadeMaxParts)
+    return fail(CS_ERR_UNSUPPORTED, "%d partials per row (max %d): max_shared_len / 512 + "
+                "max_rest_len / 1024 too large", geo.chunks + geo.segments, cs::kCascadeMaxParts);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (debug_checks_enabled()) {
     int st = debug_check_decode(block_tables, seq_lens, batch, max_seq_len, max_blocks_per_seq,
                                 num_blocks, s);
     if (st == CS_OK)
       st = debug_check_groups(block_tables, seq_lens, cu_groups, shared_lens, batch, num_groups,
-                              max_group_seqs, max_shared_len, max_blocks_per_seq, s);
+                              max_group_seqs, max_shared_len, max_rest_len, max_blocks_per_seq, s);
     if (st != CS_OK) return st;
   }
   cs::CascadeLaunch a;
@@ -457,12 +470,13 @@ int cs_cascade_decode_attn(const void* q, const void* k_pool, const void* v_pool
   a.shared_lens = shared_lens;
   a.out = static_cast<uint16_t*>(out);
   a.ws_o = static_cast<float*>(workspace);
-  a.ws_ml = a.ws_o + (size_t)geo.chunks * batch * num_q_heads * head_dim;
+  a.ws_ml = a.ws_o + (size_t)(geo.chunks + geo.segments) * batch * num_q_heads * head_dim;
   a.batch = batch;
   a.max_blocks_per_seq = max_blocks_per_seq;
   a.num_groups = num_groups;
   a.max_group_seqs = max_group_seqs;
   a.max_shared_len = max_shared_len;
+  a.max_rest_len = max_rest_len;
   a.num_q_heads = num_q_heads;
   a.num_kv_heads = num_kv_heads;
   a.head_dim = head_dim;

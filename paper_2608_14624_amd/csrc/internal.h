@@ -95,19 +95,24 @@ hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream);
 // Cascade decode: the shared prefix of each group of sequences is attended
 // once with the group's queries stacked (prefill kernel, stacked mode), in
 // chunks of kCascadeChunkSteps * 64 keys whose partial results go to a
-// workspace; the decode kernel then attends each sequence's own keys and
-// merges the partials.
+// workspace; the decode kernel attends each sequence's own keys in segments
+// of kCascadeSegmentKeys, also as partials; a merge kernel combines them.
 constexpr int kCascadeChunkSteps = 8;
+// keys of a sequence's own part per work-group of the rest-of-sequence launch
+constexpr int kCascadeSegmentKeys = 1024;
+// partials per row the merge stages in LDS (16 heads x 512 x 8 B = 64 KiB)
+constexpr int kCascadeMaxParts = 512;
 
 struct CascadeGeometry {
   int chunk_keys;     // keys per chunk of a shared prefix
   int chunks;         // chunks of the longest shared prefix
+  int segments;       // own-key segments of the longest rest of a sequence
   int row_tiles;      // 128-row tiles of the largest group
   long long grid;     // work-groups of the shared-prefix launch
 };
 
 CascadeGeometry cascade_geometry(int num_groups, int max_group_seqs, int max_shared_len,
-                                 int num_q_heads, int num_kv_heads);
+                                 int max_rest_len, int num_q_heads, int num_kv_heads);
 
 struct CascadeLaunch {
   const uint16_t* q;        // [batch][num_q_heads][head_dim]
@@ -118,13 +123,14 @@ struct CascadeLaunch {
   const int32_t* cu_groups;     // [num_groups + 1]
   const int32_t* shared_lens;   // [num_groups]
   uint16_t* out;
-  float* ws_o;                  // [chunks][batch * num_q_heads][head_dim]
-  float* ws_ml;                 // [chunks][batch * num_q_heads][2]
+  float* ws_o;                  // [chunks + segments][batch * num_q_heads][head_dim]
+  float* ws_ml;                 // [chunks + segments][batch * num_q_heads][2]
   int batch;
   int max_blocks_per_seq;
   int num_groups;
   int max_group_seqs;
   int max_shared_len;
+  int max_rest_len;
   int num_q_heads;
   int num_kv_heads;
   int head_dim;

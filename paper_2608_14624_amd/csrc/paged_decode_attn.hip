@@ -25,11 +25,13 @@
 //   * Work-groups are ordered KV head fastest, so each XCD serves one head.
 //
 // Cascade mode: a sequence belongs to a group whose shared prefix (its first
-// shared_len keys) was already attended by the stacked prefill kernel, which
-// left one partial result (O relative to its running max m, the max m and
-// the sum l) per 512-key chunk in a workspace.  The kernel then attends only
-// the sequence's own keys shared_len .. L - 1 and merges those partials with
-// its four waves' ones, all with log-sum-exp weights exp2((m_i - max) * c).
+// shared_len keys) is attended by the stacked prefill kernel, which leaves
+// one partial result (O relative to its running max m, the max m and the sum
+// l) per 512-key chunk in a workspace.  Here a work-group takes one KV head
+// and one 1024-key segment of a sequence's own keys shared_len .. L - 1, so
+// a long history spreads over several work-groups, and leaves its partial
+// in the workspace too; cascade_merge_kernel then combines every partial of
+// a row with log-sum-exp weights exp2((m_i - max) * c).
 #include "internal.h"
 
 #include <math.h>
@@ -66,11 +68,24 @@ struct DecParams {
   const int32_t* cu_groups;     // [num_groups + 1], cu_groups[0] = 0, last = batch
   const int32_t* shared_lens;   // [num_groups]
   int num_groups;
+  int batch;
   int chunk_keys;               // keys per partial of the shared prefix
-  const float* ws_o;            // [chunks][batch * num_q_heads][D]
-  const float* ws_ml;           // [chunks][batch * num_q_heads][2]
+  int chunks;                   // shared-prefix partials per row (upper bound)
+  int segments;                 // own-key partials per row (upper bound)
+  float* ws_o;                  // [chunks + segments][batch * num_q_heads][D]
+  float* ws_ml;                 // [chunks + segments][batch * num_q_heads][2]
   int ws_rows;
 };
+
+// first key of sequence r that its group does not share
+__device__ __forceinline__ int shared_len_of(const DecParams& p, int r) {
+  int lo = 0, hi = p.num_groups - 1;   // the last group gr with cu_groups[gr] <= r
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (p.cu_groups[mid] <= r) lo = mid; else hi = mid - 1;
+  }
+  return p.shared_lens[lo];
+}
 
 template <int D>
 struct DecLds {
@@ -104,26 +119,24 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
   const int qd = lane >> 4;          // lane group: k-slots 8*qd .. +7
 
   const int g = blockIdx.x % p.num_kv_heads;
-  const int r = blockIdx.x / p.num_kv_heads;
-  const int L = p.seq_lens[r];
-  const int n_blk = (L + kBlock - 1) / kBlock;
-  const int n_chunks = (L + kChunk - 1) / kChunk;
-  int start = 0;       // first key this kernel attends
-  int n_parts = 0;     // partial results of the shared prefix to merge
+  int r, seg = 0;
   if constexpr (kCascade) {
-    // the sequence's group: the last gr with cu_groups[gr] <= r
-    int lo = 0, hi = p.num_groups - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (p.cu_groups[mid] <= r) lo = mid; else hi = mid - 1;
-    }
-    start = p.shared_lens[lo];
-    n_parts = (start + p.chunk_keys - 1) / p.chunk_keys;
+    r = (blockIdx.x / p.num_kv_heads) % p.batch;
+    seg = blockIdx.x / p.num_kv_heads / p.batch;
+  } else {
+    r = blockIdx.x / p.num_kv_heads;
   }
+  const int L = p.seq_lens[r];
+  int start = 0;       // keys start .. end - 1 are this work-group's
+  int end = L;
+  if constexpr (kCascade) {
+    start = shared_len_of(p, r) + seg * kCascadeSegmentKeys;
+    end = min(L, start + kCascadeSegmentKeys);
+    if (start >= end) return;          // nothing of this sequence's own here
+  }
+  const int n_blk = (end + kBlock - 1) / kBlock;
   const int first_chunk = start / kChunk;
-  // no chunk when the shared prefix covers the whole sequence (a chunk with
-  // no visible key would turn the running max into -inf - -inf)
-  const int ch_end = start < L ? n_chunks : first_chunk;
+  const int ch_end = (end + kChunk - 1) / kChunk;
   const size_t tile_elems = (size_t)kBlock * D;
   const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
   const uint16_t* kbase = p.k_pool + (size_t)g * tile_elems;
@@ -220,7 +233,7 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int key = kbase_idx + 16 * mt + 4 * qd + rr;
-        s[mt][rr] = (key < L && key >= start) ? s[mt][rr] : -INFINITY;
+        s[mt][rr] = (key < end && key >= start) ? s[mt][rr] : -INFINITY;
         mloc = fmaxf(mloc, s[mt][rr]);
       }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
@@ -268,7 +281,6 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
     float mx = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) mx = fmaxf(mx, sm.merge.m[w][hj]);
-    for (int pc = 0; pc < n_parts; ++pc) mx = fmaxf(mx, p.ws_ml[2 * ((size_t)pc * p.ws_rows + row)]);
     float num = 0.f, den = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
@@ -276,13 +288,77 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
       num += wt * sm.merge.o[w][hj][d];
       den += wt * sm.merge.l[w][hj];
     }
-    for (int pc = 0; pc < n_parts; ++pc) {
-      const size_t widx = (size_t)pc * p.ws_rows + row;
-      const float wt = __builtin_amdgcn_exp2f((p.ws_ml[2 * widx] - mx) * c);
-      num += wt * p.ws_o[widx * D + d];
-      den += wt * p.ws_ml[2 * widx + 1];
+    if constexpr (kCascade) {
+      // this segment's partial: O relative to mx, mx, and the sum
+      const size_t widx = (size_t)(p.chunks + seg) * p.ws_rows + row;
+      p.ws_o[widx * D + d] = num;
+      if (d == 0) {
+        p.ws_ml[2 * widx] = mx;
+        p.ws_ml[2 * widx + 1] = den;
+      }
+    } else {
+      p.out[row * D + d] = __builtin_bit_cast(uint16_t, (__bf16)(num / den));
     }
-    p.out[row * D + d] = __builtin_bit_cast(uint16_t, (__bf16)(num / den));
+  }
+}
+
+// One work-group per (sequence, KV head): the final output of cascade decode
+// from every partial of the row (shared-prefix chunks, own-key segments).
+// The maxima and sums of all partials are gathered into LDS by all threads
+// at once, turned into per-partial weights, and every thread then sums its
+// output elements over the partials with the loads issued together.
+template <int D>
+__global__ __launch_bounds__(kThreads) void cascade_merge_kernel(DecParams p) {
+  extern __shared__ float wsm[];            // [group][parts]: maxima, then weights
+  const int g = blockIdx.x % p.num_kv_heads;
+  const int r = blockIdx.x / p.num_kv_heads;
+  const int L = p.seq_lens[r];
+  const int shared = shared_len_of(p, r);
+  const int n_shared = (shared + p.chunk_keys - 1) / p.chunk_keys;
+  const int n_own = (L - shared + kCascadeSegmentKeys - 1) / kCascadeSegmentKeys;
+  const int n = n_shared + n_own;
+  const int stride = p.chunks + p.segments;     // row length of wsm
+  float* m_s = wsm;
+  float* l_s = wsm + p.group * stride;
+  const float c = p.scale_log2;
+  const size_t row0 = (size_t)r * p.num_q_heads + g * p.group;
+  auto part_of = [&](int i) { return i < n_shared ? i : p.chunks + (i - n_shared); };
+  for (int t = threadIdx.x; t < p.group * n; t += kThreads) {
+    const int hj = t / n, i = t % n;
+    const float2 ml = *reinterpret_cast<const float2*>(p.ws_ml + 2 * ((size_t)part_of(i) * p.ws_rows + row0 + hj));
+    m_s[hj * stride + i] = ml.x;
+    l_s[hj * stride + i] = ml.y;
+  }
+  __syncthreads();
+  if (threadIdx.x < p.group) {
+    const int hj = threadIdx.x;
+    float mx = -INFINITY;
+    for (int i = 0; i < n; ++i) mx = fmaxf(mx, m_s[hj * stride + i]);
+    float den = 0.f;
+    for (int i = 0; i < n; ++i) {
+      const float wt = __builtin_amdgcn_exp2f((m_s[hj * stride + i] - mx) * c);
+      m_s[hj * stride + i] = wt;              // the maximum becomes the weight
+      den += wt * l_s[hj * stride + i];
+    }
+    const float inv = 1.f / den;
+    for (int i = 0; i < n; ++i) m_s[hj * stride + i] *= inv;
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < p.group * D; idx += kThreads) {
+    const int hj = idx / D;
+    const int d = idx % D;
+    const size_t row = row0 + hj;
+    float acc = 0.f;
+    int i = 0;
+    for (; i + 4 <= n; i += 4) {
+      float o[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) o[u] = p.ws_o[((size_t)part_of(i + u) * p.ws_rows + row) * D + d];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc += m_s[hj * stride + i + u] * o[u];
+    }
+    for (; i < n; ++i) acc += m_s[hj * stride + i] * p.ws_o[((size_t)part_of(i) * p.ws_rows + row) * D + d];
+    p.out[row * D + d] = __builtin_bit_cast(uint16_t, (__bf16)acc);
   }
 }
 
@@ -311,6 +387,8 @@ hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream) {
 }
 
 hipError_t launch_cascade_decode_rest(const CascadeLaunch& a, hipStream_t stream) {
+  const CascadeGeometry geo = cascade_geometry(a.num_groups, a.max_group_seqs, a.max_shared_len,
+                                               a.max_rest_len, a.num_q_heads, a.num_kv_heads);
   DecParams p = {};
   p.q = a.q;
   p.k_pool = a.k_pool;
@@ -326,15 +404,29 @@ hipError_t launch_cascade_decode_rest(const CascadeLaunch& a, hipStream_t stream
   p.cu_groups = a.cu_groups;
   p.shared_lens = a.shared_lens;
   p.num_groups = a.num_groups;
-  p.chunk_keys = kCascadeChunkSteps * 64;
+  p.batch = a.batch;
+  p.chunk_keys = geo.chunk_keys;
+  p.chunks = geo.chunks;
+  p.segments = geo.segments;
   p.ws_o = a.ws_o;
   p.ws_ml = a.ws_ml;
   p.ws_rows = a.batch * a.num_q_heads;
-  const dim3 grid((unsigned)((long long)a.batch * a.num_kv_heads)), block(kThreads);
+  const long long rows = (long long)a.batch * a.num_kv_heads;
+  if (geo.segments > 0) {
+    const dim3 grid((unsigned)(rows * geo.segments)), block(kThreads);
+    if (a.head_dim == 128) {
+      hipLaunchKernelGGL((paged_decode_attn_kernel<128, true>), grid, block, 0, stream, p);
+    } else {
+      hipLaunchKernelGGL((paged_decode_attn_kernel<64, true>), grid, block, 0, stream, p);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const size_t lds = 2 * sizeof(float) * (size_t)p.group * (geo.chunks + geo.segments);
   if (a.head_dim == 128) {
-    hipLaunchKernelGGL((paged_decode_attn_kernel<128, true>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL(cascade_merge_kernel<128>, dim3((unsigned)rows), dim3(kThreads), lds, stream, p);
   } else {
-    hipLaunchKernelGGL((paged_decode_attn_kernel<64, true>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL(cascade_merge_kernel<64>, dim3((unsigned)rows), dim3(kThreads), lds, stream, p);
   }
   return hipGetLastError();
 }

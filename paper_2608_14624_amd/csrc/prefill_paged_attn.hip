@@ -812,11 +812,12 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
 }
 
 CascadeGeometry cascade_geometry(int num_groups, int max_group_seqs, int max_shared_len,
-                                 int num_q_heads, int num_kv_heads) {
+                                 int max_rest_len, int num_q_heads, int num_kv_heads) {
   CascadeGeometry geo;
   const int group = num_q_heads / num_kv_heads;
   geo.chunk_keys = kCascadeChunkSteps * kBN;
   geo.chunks = (max_shared_len + geo.chunk_keys - 1) / geo.chunk_keys;
+  geo.segments = (max_rest_len + kCascadeSegmentKeys - 1) / kCascadeSegmentKeys;
   geo.row_tiles = ((long long)max_group_seqs * group + kRowsPerWG - 1) / kRowsPerWG;
   geo.grid = (long long)num_kv_heads * geo.row_tiles * geo.chunks * num_groups;
   return geo;
@@ -824,7 +825,7 @@ CascadeGeometry cascade_geometry(int num_groups, int max_group_seqs, int max_sha
 
 hipError_t launch_shared_prefix_partials(const CascadeLaunch& a, hipStream_t stream) {
   const CascadeGeometry geo = cascade_geometry(a.num_groups, a.max_group_seqs, a.max_shared_len,
-                                               a.num_q_heads, a.num_kv_heads);
+                                               a.max_rest_len, a.num_q_heads, a.num_kv_heads);
   if (geo.grid == 0) return hipSuccess;
   Params p = {};
   p.q = a.q;

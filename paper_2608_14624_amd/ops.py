@@ -64,10 +64,10 @@ def _load():
                                          i32, f32, vp, vp]
     lib.cs_paged_decode_attn.restype = ctypes.c_int
     lib.cs_cascade_decode_attn.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp, i32,
-                                           i32, i32, i32, i32, i32, i32, f32, vp,
+                                           i32, i32, i32, i32, i32, i32, i32, f32, vp,
                                            ctypes.c_int64, vp, vp]
     lib.cs_cascade_decode_attn.restype = ctypes.c_int
-    lib.cs_cascade_decode_workspace_bytes.argtypes = [i32, i32, i32, i32]
+    lib.cs_cascade_decode_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
     lib.cs_cascade_decode_workspace_bytes.restype = ctypes.c_int64
     lib.cs_status_string.argtypes = [ctypes.c_int]
     lib.cs_status_string.restype = ctypes.c_char_p
@@ -317,25 +317,26 @@ def cs_paged_decode_attn(q, k_pool, v_pool, block_tables, seq_lens, out, *, max_
 
 def cs_cascade_decode_attn_raw(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
                                max_blocks_per_seq, num_blocks, cu_groups, shared_lens, num_groups,
-                               max_group_seqs, max_shared_len, num_q_heads, num_kv_heads, head_dim,
-                               block_size, scale, workspace, workspace_bytes, out, stream=0):
+                               max_group_seqs, max_shared_len, max_rest_len, num_q_heads,
+                               num_kv_heads, head_dim, block_size, scale, workspace,
+                               workspace_bytes, out, stream=0):
     """The C call with raw pointers (ints or None); returns the status code."""
     return _lib.cs_cascade_decode_attn(q, k_pool, v_pool, block_tables, seq_lens, batch,
                                        max_seq_len, max_blocks_per_seq, num_blocks, cu_groups,
                                        shared_lens, num_groups, max_group_seqs, max_shared_len,
-                                       num_q_heads, num_kv_heads, head_dim, block_size,
-                                       ctypes.c_float(scale), workspace, workspace_bytes, out,
-                                       stream)
+                                       max_rest_len, num_q_heads, num_kv_heads, head_dim,
+                                       block_size, ctypes.c_float(scale), workspace,
+                                       workspace_bytes, out, stream)
 
 
-def cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim, max_shared_len):
+def cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim, max_shared_len, max_rest_len):
     return int(_lib.cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim,
-                                                      max_shared_len))
+                                                      max_shared_len, max_rest_len))
 
 
 def cs_cascade_decode_attn(q, k_pool, v_pool, block_tables, seq_lens, cu_groups, shared_lens,
-                           out, *, max_seq_len, max_group_seqs, max_shared_len, scale,
-                           workspace=None, stream=None):
+                           out, *, max_seq_len, max_group_seqs, max_shared_len, max_rest_len,
+                           scale, workspace=None, stream=None):
     """Enqueue cascade decode attention.  Tensors as for
     :func:`cs_paged_decode_attn`, plus ``cu_groups`` int32 ``[G+1]`` and
     ``shared_lens`` int32 ``[G]`` on the device.  ``workspace``: a uint8 GPU
@@ -359,14 +360,15 @@ def cs_cascade_decode_attn(q, k_pool, v_pool, block_tables, seq_lens, cu_groups,
     _require(seq_lens.numel() == batch, "seq_lens must have B entries")
     num_groups = shared_lens.numel()
     _require(cu_groups.numel() == num_groups + 1, "cu_groups must have G + 1 entries")
-    need = cs_cascade_decode_workspace_bytes(batch, hq, d, int(max_shared_len))
+    need = cs_cascade_decode_workspace_bytes(batch, hq, d, int(max_shared_len), int(max_rest_len))
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
     _require(workspace.is_cuda and workspace.device == dev, f"workspace must be on {dev}")
     _check(cs_cascade_decode_attn_raw(
         _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_tables), _ptr(seq_lens), batch,
         int(max_seq_len), block_tables.shape[1], num_blocks, _ptr(cu_groups), _ptr(shared_lens),
-        num_groups, int(max_group_seqs), int(max_shared_len), hq, hkv, d, bs, float(scale),
+        num_groups, int(max_group_seqs), int(max_shared_len), int(max_rest_len), hq, hkv, d, bs,
+        float(scale),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(out),
         _stream_handle(stream, dev)))
 

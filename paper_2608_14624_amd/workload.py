@@ -456,7 +456,8 @@ def cascade_view(wl):
     nothing.  Returns a dict with ``order`` (the batch permutation: row ``i``
     of the grouped batch is sequence ``order[i]``), ``cu_groups``,
     ``shared_lens``, ``max_group_seqs`` (over groups that share something, at
-    least 1) and ``max_shared_len``.
+    least 1), ``max_shared_len`` and ``max_rest_len`` (the most keys of its
+    own any sequence has beyond its group's shared part).
     """
     bs = wl.block_size
     by_agent = {}
@@ -476,11 +477,15 @@ def cascade_view(wl):
         cu.append(len(order))
         shared.append(0)
     sizes = [cu[i + 1] - cu[i] for i in range(len(shared)) if shared[i] > 0]
+    kv = wl.kv_lens
+    rest = [int(kv[order[k]]) - shared[gi] for gi in range(len(shared))
+            for k in range(cu[gi], cu[gi + 1])]
     return dict(order=np.asarray(order, dtype=np.int64),
                 cu_groups=np.asarray(cu, dtype=np.int32),
                 shared_lens=np.asarray(shared, dtype=np.int32),
                 max_group_seqs=max(sizes + [1]),
-                max_shared_len=max(shared + [0]))
+                max_shared_len=max(shared + [0]),
+                max_rest_len=max(rest + [0]))
 
 
 def make_config(name):

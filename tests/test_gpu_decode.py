@@ -112,7 +112,13 @@ def grouped_batch(wl):
             np.ascontiguousarray(wl.block_tables[o]), cv)
 
 
-def run_cascade(wl, q, seq_lens, bt, cu, shared, max_group_seqs, max_shared_len, workspace=None):
+def rest_bound(seq_lens, cu, shared):
+    return max(int(seq_lens[r]) - int(shared[g]) for g in range(len(shared))
+               for r in range(cu[g], cu[g + 1]))
+
+
+def run_cascade(wl, q, seq_lens, bt, cu, shared, max_group_seqs, max_shared_len, workspace=None,
+                max_rest_len=None):
     from paper_2608_14624_amd import ops
     qd = dev_bf16(q)
     out = torch.full_like(qd, float("nan"))
@@ -121,7 +127,10 @@ def run_cascade(wl, q, seq_lens, bt, cu, shared, max_group_seqs, max_shared_len,
                                torch.from_numpy(np.asarray(cu, np.int32)).cuda(),
                                torch.from_numpy(np.asarray(shared, np.int32)).cuda(), out,
                                max_seq_len=int(seq_lens.max()), max_group_seqs=max_group_seqs,
-                               max_shared_len=max_shared_len, scale=wl.scale, workspace=workspace)
+                               max_shared_len=max_shared_len,
+                               max_rest_len=(rest_bound(seq_lens, cu, shared)
+                                             if max_rest_len is None else max_rest_len),
+                               scale=wl.scale, workspace=workspace)
     torch.cuda.synchronize()
     return oracle.bf16_bits_to_f64(out.view(torch.int16).cpu().numpy().view(np.uint16))
 
@@ -176,6 +185,19 @@ def test_cascade_decode_two_row_tiles_and_empty_private_part():
     check(got, oracle_decode(q, seq_lens, bt, wl), "vs oracle")
 
 
+def test_cascade_decode_long_own_parts_span_several_segments():
+    # own parts of 1023, 1024, 1025 and 3000 keys: one to three 1024-key
+    # segments, ragged ends, next to a group that shares 2048 keys
+    invs = [Invocation(0, s) for s in (1023, 1024, 1025, 3000)] + [Invocation(1, 7)]
+    wl = build_workload("segs", 44, [2048, 96], invs, num_q_heads=16, num_kv_heads=4,
+                        head_dim=128, num_blocks=2048)
+    q, seq_lens, bt, cv = grouped_batch(wl)
+    print(f"[case] cascade segments: rest={cv['max_rest_len']}", flush=True)
+    got = run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"],
+                      cv["max_group_seqs"], cv["max_shared_len"])
+    check(got, oracle_decode(q, seq_lens, bt, wl), "vs oracle")
+
+
 def test_cascade_decode_without_sharing_equals_paged_decode():
     anchors, spec, hq, hkv, d = CASCADE_CASES["mixed_g4"]
     invs = [Invocation(a, s, h) for a, s, h in spec]
@@ -184,8 +206,13 @@ def test_cascade_decode_without_sharing_equals_paged_decode():
     q, seq_lens = decode_view(wl)
     got = run_cascade(wl, q, seq_lens, wl.block_tables, [0, wl.batch], [0], 1, 0)
     ref = run_decode(wl)
-    # one group sharing nothing runs exactly the paged decode kernel's loop
-    assert np.array_equal(got, ref)
+    # one group sharing nothing: a sequence of at most one 1024-key segment
+    # runs exactly the paged decode kernel's loop and merge; longer ones are
+    # merged across segments, equal up to rounding
+    single = seq_lens <= 1024
+    assert single.any() and (~single).any()
+    assert np.array_equal(got[single], ref[single])
+    check(got, oracle_decode(q, seq_lens, wl.block_tables, wl), "vs oracle")
 
 
 def test_cascade_decode_batch_config():
@@ -204,7 +231,8 @@ def test_cascade_workspace_reuse_and_debug_checks(monkeypatch):
     wl = build_workload("dbg", 41, anchors, invs, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
                         num_blocks=1024)
     q, seq_lens, bt, cv = grouped_batch(wl)
-    need = ops.cs_cascade_decode_workspace_bytes(wl.batch, hq, d, cv["max_shared_len"])
+    need = ops.cs_cascade_decode_workspace_bytes(wl.batch, hq, d, cv["max_shared_len"],
+                                                 cv["max_rest_len"])
     ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")   # NaN-filled scratch
     args = (wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"], cv["max_group_seqs"],
             cv["max_shared_len"])
@@ -222,3 +250,6 @@ def test_cascade_workspace_reuse_and_debug_checks(monkeypatch):
     with pytest.raises(ops.CacheScoutError, match="max_group_seqs"):
         run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"], 1,
                     cv["max_shared_len"], workspace=ws)
+    with pytest.raises(ops.CacheScoutError, match="max_rest_len"):
+        run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"], cv["max_group_seqs"],
+                    cv["max_shared_len"], workspace=ws, max_rest_len=cv["max_rest_len"] - 1)
