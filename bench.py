@@ -78,15 +78,16 @@ def load_traffic(kernel, workload, kernel_hash):
 
 def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim):
     """Which attention kernel a launch runs: the 8-wave ping-pong kernel when
-    its grid has at least one work-group per CU (256), else the four-wave one
-    (the library's launch rule, repeated here only to label the result)."""
+    its grid has at least one work-group per CU (256), else the split
+    four-wave-tile one (the library's launch rule, repeated here only to label
+    the result)."""
     group = num_q_heads // num_kv_heads
     hw = 4 if group % 4 == 0 else 2 if group % 2 == 0 else 1
     span = 32 * (8 // hw)
     grid = -(-max_q_len // span) * batch * (num_q_heads // hw)
     if grid >= 256:
         return f"prefill_paged_attn_pp_kernel<{head_dim}>"
-    return f"prefill_paged_attn_kernel<{head_dim}, false>"
+    return f"prefill_paged_attn_kernel<{head_dim}, false, true>"
 
 
 def cpu_baseline(wl, budget_s=20.0):
@@ -226,7 +227,7 @@ def bench_copy(args, dev):
     kernel, sources = {
         "decode": ("paged_decode_attn_kernel<128, false>",
                    ("paper_2608_14624_amd/csrc/paged_decode_attn.hip",)),
-        "cascade_decode": ("prefill_paged_attn_kernel<128, true> + paged_decode_attn_kernel<128, true>"
+        "cascade_decode": ("prefill_paged_attn_kernel<128, true, false> + paged_decode_attn_kernel<128, true>"
                            " + cascade_merge_kernel<128>",
                            ("paper_2608_14624_amd/csrc/prefill_paged_attn.hip",
                             "paper_2608_14624_amd/csrc/paged_decode_attn.hip")),

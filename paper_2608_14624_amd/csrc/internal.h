@@ -26,7 +26,8 @@ struct AttnLaunch {
 
 // Launch geometry of the attention kernel (host-side, for tests and tuning).
 struct AttnGeometry {
-  int waves;          // waves per work-group: 8 (ping-pong kernel) or 4
+  int waves;          // row waves per work-group: 8 (ping-pong kernel), or 4
+                      // (each tile run by 8 waves over two halves of its keys)
   int heads_per_wg;   // query heads of one GQA group handled by one work-group
   int span;           // suffix tokens handled by one work-group
   int token_tiles;    // span-sized token tiles per invocation (upper bound)

@@ -41,6 +41,14 @@
 // K/V tiles serve 8 waves instead of 4 (waves 0-3 stage K, 4-7 stage V), and
 // each row's arithmetic is the same as in the four-wave kernel, bit for bit.
 //
+// Split launches (fewer than one ping-pong work-group per CU): a four-wave
+// tile alone on a CU would leave one wave per SIMD, with nothing to hide its
+// softmax behind.  Instead 8 waves run each 128-row tile: waves w and w + 4
+// own the same rows, waves 0-3 take the first half of the key steps and
+// waves 4-7 the second, each half with its own LDS buffers (two halves of
+// 74 KiB for D = 128), and at the end waves 4-7 hand (O, m, l) to waves 0-3
+// through LDS, which merge them with the log-sum-exp weights.
+//
 // Stacked mode (the shared-prefix half of cascade attention): the query rows
 // of a work-group are any 128 (sequence, query head) pairs of one group of
 // sequences that share a prefix and one KV head; they attend, without a
@@ -144,9 +152,13 @@ __device__ __forceinline__ float pair_sum(float x) {
 
 constexpr int kRowsPerWG = kNQ * kWaves;
 
-template <int D, bool kStacked>
-__global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) {
-  __shared__ Lds<D> sm;
+// kSplit: 8 waves; waves w and w + 4 own the same 32 rows, waves 0-3 take
+// the first half of the key steps and waves 4-7 the second, each half with
+// its own LDS buffers; the halves are merged through LDS at the end.  For
+// launches too small for two work-groups per CU.
+template <int D, bool kStacked, bool kSplit>
+__global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_paged_attn_kernel(Params p) {
+  __shared__ Lds<D> sm_all[kSplit ? 2 : 1];
   constexpr int kStride = Lds<D>::kStride;
   constexpr int vStride = Lds<D>::vStride;
   constexpr int KS = D / 16;     // MFMA k-steps over the head dim
@@ -154,7 +166,9 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = (tid >> 6) & 3;            // row owner within the work-group
+  const int split_half = kSplit ? __builtin_amdgcn_readfirstlane(tid >> 8) : 0;
+  Lds<D>& sm = sm_all[split_half];
   const int qi = lane & 31;
   const int half = lane >> 5;
 
@@ -226,6 +240,14 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     n_blk = SH / kBlock;
     bt = p.block_tables + (size_t)s0 * p.max_blocks_per_seq;   // the group's shared blocks
     wave_qmin = ke - 1;
+  }
+  // split mode: this half's steps; both halves run n_iter iterations so
+  // that their barriers match
+  const int n_iter = kSplit ? n_steps - n_steps / 2 : n_steps;
+  if constexpr (kSplit) {
+    const int first = split_half ? n_steps / 2 : 0;
+    n_steps = split_half ? n_steps - n_steps / 2 : n_steps / 2;
+    j0 += first;
   }
   const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
   const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
@@ -350,6 +372,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     const int kstart = (j0 + j) * kBN;
     const int cur = j & 1;
     __syncthreads();   // iteration j-1's reads are done and its writes visible
+    if (kSplit && j >= n_steps) return;            // this half is done; keep the barriers
     if (j + 1 < n_steps) {
       store_tile(kst, sm.k[cur ^ 1], kStride);     // K_{j+1}, V_{j+1}
       store_tile(vst, sm.v[cur ^ 1], vStride);
@@ -391,10 +414,12 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
     mloc = pair_max(mloc);
     // ---- lazy rescale: move the reference max only when a row's max grew
     // by more than 2^8 in probability; otherwise keep it (p <= 256 then)
+    // (a row whose keys so far were all masked keeps m_run = -inf: possible
+    // only for the second half of a split work-group)
     const bool grow = (mloc - m_run) * c > 8.f;      // true for every row at step 0
     if (__builtin_amdgcn_ballot_w64(grow) != 0) {
       const float m_new = grow ? mloc : m_run;
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      const float alpha = (kSplit && m_new == m_run) ? 1.f : __builtin_amdgcn_exp2f((m_run - m_new) * c);
       m_run = m_new;
 #pragma unroll
       for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
@@ -402,7 +427,7 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
       for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
     }
 
-    const float mc = m_run * c;
+    const float mc = (kSplit && m_run == -INFINITY) ? 0.f : m_run * c;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -435,13 +460,41 @@ __global__ __launch_bounds__(kThreads) void prefill_paged_attn_kernel(Params p) 
   };
 
   // unrolled by two so the register stage of each step is a constant
-  for (int j = 0; j < n_steps; j += 2) {
+  for (int j = 0; j < n_iter; j += 2) {
     step(j, kreg[1], vreg[1]);
-    if (j + 1 < n_steps) step(j + 1, kreg[0], vreg[0]);
+    if (j + 1 < n_iter) step(j + 1, kreg[0], vreg[0]);
   }
   const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
 
-  const float l_tot = pair_sum(l_run);
+  float l_tot = pair_sum(l_run);
+  if constexpr (kSplit) {
+    // waves 4-7 hand (O, m, l) of their rows to waves 0-3 through the second
+    // half's LDS, which every wave has finished reading; value e of lane l
+    // of wave w sits at word e * 256 + 64 w + l (no bank conflicts)
+    constexpr int kX = DT * 16 + 2;
+    static_assert(kX * 256 * sizeof(float) <= sizeof(Lds<D>), "exchange exceeds one LDS half");
+    float* x = reinterpret_cast<float*>(&sm_all[kSplit ? 1 : 0]) + wave * 64 + lane;
+    __syncthreads();
+    if (split_half == 1) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) x[(dt * 16 + rr) * 256] = oacc[dt][rr];
+      x[DT * 16 * 256] = m_run;
+      x[(DT * 16 + 1) * 256] = l_tot;
+    }
+    __syncthreads();
+    if (split_half == 1) return;
+    const float m1 = x[DT * 16 * 256];
+    const float mx = fmaxf(m_run, m1);
+    const float w0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run - mx) * c);
+    const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m1 - mx) * c);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) oacc[dt][rr] = w0 * oacc[dt][rr] + w1 * x[(dt * 16 + rr) * 256];
+    l_tot = w0 * l_tot + w1 * x[(DT * 16 + 1) * 256];
+  }
   if constexpr (kStacked) {
     // ---- partial result: O (relative to m_run), m_run, l -----------
     if (row_valid) {
@@ -804,9 +857,11 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
       hipLaunchKernelGGL(prefill_paged_attn_pp_kernel<64>, grid, dim3(kPPThreads), 0, stream, p);
     }
   } else if (a.head_dim == 128) {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, false>), grid, dim3(kThreads), 0, stream, p);
+    // fewer than one ping-pong work-group per CU: 128-row tiles, each run
+    // by 8 waves over two halves of its keys
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, false, true>), grid, dim3(2 * kThreads), 0, stream, p);
   } else {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, false>), grid, dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, false, true>), grid, dim3(2 * kThreads), 0, stream, p);
   }
   return hipGetLastError();
 }
@@ -848,9 +903,9 @@ hipError_t launch_shared_prefix_partials(const CascadeLaunch& a, hipStream_t str
   p.ws_rows = a.batch * a.num_q_heads;
   const dim3 grid((unsigned)geo.grid), block(kThreads);
   if (a.head_dim == 128) {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, true>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, true, false>), grid, block, 0, stream, p);
   } else {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, true>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, true, false>), grid, block, 0, stream, p);
   }
   return hipGetLastError();
 }

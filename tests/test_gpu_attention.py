@@ -75,6 +75,12 @@ EDGE = {
     "zero_prefix_hit": ([0], [Invocation(0, 77)], 8, 2, 128, {}),
     "peaky_logits": ([90], [Invocation(0, 70)], 8, 2, 128, {"q_gain": 8.0}),
     "long_ragged_tile": ([1000], [Invocation(0, 257), Invocation(0, 129)], 32, 8, 128, {}),
+    # small launches split each tile's key steps over two wave groups: one
+    # step (the first group has none), rows whose keys in the second group's
+    # half are all masked, and a long prefix under a short suffix
+    "split_one_key": ([0], [Invocation(0, 1)], 8, 2, 128, {}),
+    "split_masked_second_half": ([0], [Invocation(0, 65), Invocation(0, 130)], 8, 2, 128, {}),
+    "split_long_prefix_short_suffix": ([1000], [Invocation(0, 3)], 8, 1, 64, {}),
 }
 
 
@@ -199,11 +205,11 @@ def test_run_to_run_determinism(P):
 
 
 @pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 8, 64), (12, 4, 128), (8, 8, 128)])
-def test_wide_and_four_wave_kernels_agree_bitwise(P, hq, hkv, d):
+def test_wide_and_small_launches_agree(P, hq, hkv, d):
     """A batch large enough for the 8-wave ping-pong kernel, and its first
-    invocation alone (a launch below one work-group per CU, which takes the
-    four-wave kernel), give bit-identical rows: each row's arithmetic is the
-    same in both."""
+    invocation alone (a launch below one work-group per CU, whose tiles run
+    with their key steps split over two wave groups), agree to the parity
+    tolerance, and the batch matches the oracle."""
     _, pipeline = P
     invs = [Invocation(i % 3, 300 + 37 * i) for i in range(16)]
     wl = build_workload("wide", 12, [520, 77, 1200], invs, num_q_heads=hq, num_kv_heads=hkv,
@@ -219,7 +225,10 @@ def test_wide_and_four_wave_kernels_agree_bitwise(P, hq, hkv, d):
                               max_q_len=first.max_q_len, max_kv_len=first.max_kv_len,
                               scale=wl.scale)
     torch.cuda.synchronize()
-    assert torch.equal(alone.view(torch.int16), first.out.view(torch.int16))
+    diff = (alone.float() - first.out.float()).abs()
+    print(f"    alone vs batch: max_abs={diff.max().item():.3e} mean_abs={diff.mean().item():.3e}",
+          flush=True)
+    assert diff.max().item() <= MAX_ABS and diff.mean().item() <= MEAN_ABS
     samples = sample_rows(wl, 200, seed=5)
     mx, mean = compare_rows(wl, dw.out_bits(), samples)
     print(f"    {len(samples)} rows: max_abs={mx:.3e} mean_abs={mean:.3e}", flush=True)
