@@ -77,16 +77,12 @@ def load_traffic(kernel, workload, kernel_hash):
 
 
 def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim):
-    """Which attention kernel a launch runs: the 8-wave ping-pong kernel when
-    its grid has at least one work-group per CU (256), else the split
-    four-wave-tile one (the library's launch rule, repeated here only to label
-    the result)."""
-    group = num_q_heads // num_kv_heads
-    hw = 4 if group % 4 == 0 else 2 if group % 2 == 0 else 1
-    span = 32 * (8 // hw)
-    grid = -(-max_q_len // span) * batch * (num_q_heads // hw)
-    if grid >= 256:
-        return f"prefill_paged_attn_pp_kernel<{head_dim}>"
+    """Which attention kernel a launch runs (the library's own launch rule,
+    asked through cs_prefill_paged_attn_launch_shape)."""
+    from paper_2608_14624_amd import ops
+    kernel, _, tail = ops.prefill_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads)
+    if kernel == ops.ATTN_PING_PONG:
+        return f"prefill_paged_attn_pp_kernel<{head_dim}, {'true' if tail else 'false'}>"
     return f"prefill_paged_attn_kernel<{head_dim}, false, true>"
 
 

@@ -133,6 +133,29 @@ int cs_prefill_paged_attn(const void *q, const void *k_pool, const void *v_pool,
                           cs_stream_t stream);
 
 /*
+ * Launch shape of cs_prefill_paged_attn for a batch: a host-only query (no
+ * GPU work, no device pointers) for profilers and tests that need to know
+ * which kernel a call runs.
+ *
+ *   *kernel      CS_ATTN_SPLIT: 128-row tiles, each run by 8 waves over two
+ *                halves of its keys (launches of fewer than 256 256-row
+ *                tiles, one round on the 256 CUs); CS_ATTN_PING_PONG:
+ *                256-row tiles, where the last *tail_work_groups work-groups
+ *                run the tiles of a last round at most half full as split
+ *                128-row halves.
+ *   *grid        work-groups of the launch (0 for a no-op call).
+ *   *tail_work_groups  0 unless *kernel is CS_ATTN_PING_PONG.
+ *
+ * Arguments as in cs_prefill_paged_attn; batch, max_q_len >= 0, head counts
+ * positive with num_q_heads % num_kv_heads == 0, else CS_ERR_INVALID_ARG.
+ * Output pointers must be non-null.
+ */
+enum { CS_ATTN_SPLIT = 0, CS_ATTN_PING_PONG = 1 };
+int cs_prefill_paged_attn_launch_shape(int32_t batch, int32_t max_q_len, int32_t num_q_heads,
+                                       int32_t num_kv_heads, int32_t *kernel, int64_t *grid,
+                                       int64_t *tail_work_groups);
+
+/*
  * KV prefetch: copy whole blocks from pinned host memory into pool slots.
  *
  * Operation (reload of an anchor from the CPU tier, Sec. 3 architecture

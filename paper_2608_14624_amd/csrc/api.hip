@@ -322,6 +322,21 @@ int cs_prefill_paged_attn(const void* q, const void* k_pool, const void* v_pool,
   return ok();
 }
 
+int cs_prefill_paged_attn_launch_shape(int32_t batch, int32_t max_q_len, int32_t num_q_heads,
+                                       int32_t num_kv_heads, int32_t* kernel, int64_t* grid,
+                                       int64_t* tail_work_groups) {
+  if (!kernel || !grid || !tail_work_groups) return fail(CS_ERR_INVALID_ARG, "null output pointer");
+  if (batch < 0 || max_q_len < 0) return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0)
+    return fail(CS_ERR_INVALID_ARG, "num_q_heads %d, num_kv_heads %d", num_q_heads, num_kv_heads);
+  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, num_q_heads, num_kv_heads);
+  const bool pp = geo.waves == 8;
+  *kernel = pp ? CS_ATTN_PING_PONG : CS_ATTN_SPLIT;
+  *grid = (batch == 0 || max_q_len == 0) ? 0 : geo.grid;
+  *tail_work_groups = pp && *grid ? geo.grid - geo.pp_grid : 0;
+  return ok();
+}
+
 int cs_kv_prefetch(const void* host_k_blocks, const void* host_v_blocks,
                    const int32_t* dst_block_ids, int32_t n, void* k_pool, void* v_pool,
                    int32_t num_blocks, int32_t num_kv_heads, int32_t head_dim, int32_t block_size,

@@ -33,6 +33,8 @@ struct AttnGeometry {
   int token_tiles;    // span-sized token tiles per invocation (upper bound)
   int head_tiles;     // num_q_heads / heads_per_wg
   long long grid;     // work-groups launched
+  long long pp_grid;  // ping-pong work-groups; the rest of the grid (ping-pong
+                      // launches only) runs the half tiles of the last round
 };
 
 AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads);

@@ -32,7 +32,7 @@
 // each serve one KV head and its K/V stays in that XCD's L2; token tiles are
 // issued from the last (most keys) to the first.
 //
-// Ping-pong kernel (launches with at least one work-group per CU): 8 waves,
+// Ping-pong kernel (launches of at least a round of its tiles): 8 waves,
 // 256 query rows per work-group, one work-group per CU, and the two waves of
 // a SIMD are offset by half a step: waves 0-3 run an iteration as [MFMAs:
 // PV of the previous step + QK^T of this one][softmax of this step], waves
@@ -41,13 +41,15 @@
 // K/V tiles serve 8 waves instead of 4 (waves 0-3 stage K, 4-7 stage V), and
 // each row's arithmetic is the same as in the four-wave kernel, bit for bit.
 //
-// Split launches (fewer than one ping-pong work-group per CU): a four-wave
+// Split launches (less than a round of ping-pong tiles): a four-wave
 // tile alone on a CU would leave one wave per SIMD, with nothing to hide its
 // softmax behind.  Instead 8 waves run each 128-row tile: waves w and w + 4
 // own the same rows, waves 0-3 take the first half of the key steps and
 // waves 4-7 the second, each half with its own LDS buffers (two halves of
 // 74 KiB for D = 128), and at the end waves 4-7 hand (O, m, l) to waves 0-3
-// through LDS, which merge them with the log-sum-exp weights.
+// through LDS, which merge them with the log-sum-exp weights.  A ping-pong
+// launch whose last round would be at most half full runs that round's tiles
+// the same way, as two 128-row halves each, so it occupies every CU.
 //
 // Stacked mode (the shared-prefix half of cascade attention): the query rows
 // of a work-group are any 128 (sequence, query head) pairs of one group of
@@ -79,9 +81,8 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPPWaves = 8;             // ping-pong kernel: two groups of four waves
 constexpr int kPPThreads = 64 * kPPWaves;
-// the ping-pong kernel takes a launch that has at least one work-group per CU
-// (MI355X: 256 CUs); smaller launches keep two four-wave work-groups per CU
-constexpr long long kPPMinGrid = 256;
+// CUs of an MI355X: one round of ping-pong (or split) work-groups
+constexpr long long kCUs = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct Params {
@@ -102,6 +103,10 @@ struct Params {
   int token_tiles;
   int head_tiles;
   float scale_log2;   // scale * log2(e)
+  // ping-pong launches: work-groups below pp_grid take ping-pong tiles; the
+  // rest take the two 128-row halves of the tiles pp_grid, pp_grid + 1, ...
+  // (span = the ping-pong tile's tokens)
+  long long pp_grid;
   // stacked mode only
   const int32_t* cu_groups;     // [num_groups + 1] sequence range of each group
   const int32_t* shared_lens;   // [num_groups] shared prefix tokens (multiple of 16)
@@ -155,10 +160,11 @@ constexpr int kRowsPerWG = kNQ * kWaves;
 // kSplit: 8 waves; waves w and w + 4 own the same 32 rows, waves 0-3 take
 // the first half of the key steps and waves 4-7 the second, each half with
 // its own LDS buffers; the halves are merged through LDS at the end.  For
-// launches too small for two work-groups per CU.
-template <int D, bool kStacked, bool kSplit>
-__global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_paged_attn_kernel(Params p) {
-  __shared__ Lds<D> sm_all[kSplit ? 2 : 1];
+// launches too small for two work-groups per CU, and for the tail of a
+// ping-pong launch (kTail: work-group wg takes one half of a ping-pong tile).
+template <int D, bool kStacked, bool kSplit, bool kTail>
+__device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const int wg) {
+  static_assert(!kTail || (kSplit && !kStacked), "a tail tile runs split");
   constexpr int kStride = Lds<D>::kStride;
   constexpr int vStride = Lds<D>::vStride;
   constexpr int KS = D / 16;     // MFMA k-steps over the head dim
@@ -176,7 +182,6 @@ __global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_page
   // Work-groups are dealt to the 8 XCDs round-robin, so the KV head is the
   // fastest-varying index: with 8 KV heads every XCD serves exactly one and
   // keeps its K/V in its own L2.
-  const int wg = blockIdx.x;
   int g;                // KV head
   bool row_valid;       // this lane holds a real query row
   size_t qrow;          // element offset of the row in q (and out)
@@ -191,15 +196,28 @@ __global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_page
     // the head tiles of the KV head come next, then invocations, then
     // token tiles from the last (most keys) to the first
     const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
-    g = wg % p.num_kv_heads;
-    const int sub = wg / p.num_kv_heads;
+    int tile = wg;
+    int span = p.span;
+    int sub_half = 0;
+    if constexpr (kTail) {
+      // halves of one ping-pong tile are num_kv_heads work-groups apart,
+      // so both run on the XCD that holds their KV head
+      const long long j = wg - p.pp_grid;
+      const int kv = (int)(j % p.num_kv_heads);
+      const long long rj = j / p.num_kv_heads;
+      sub_half = (int)(rj & 1);
+      tile = (int)(p.pp_grid + (rj >> 1) * p.num_kv_heads + kv);
+      span = p.span / 2;
+    }
+    g = tile % p.num_kv_heads;
+    const int sub = tile / p.num_kv_heads;
     const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
     const int rest = sub / tiles_per_kv;
     const int r = rest % p.batch;
     const int token_tile = p.token_tiles - 1 - rest / p.batch;
     const int q0 = p.cu_q_lens[r];
     const int S = p.cu_q_lens[r + 1] - q0;
-    const int t0 = token_tile * p.span;
+    const int t0 = token_tile * p.span + sub_half * span;
     if (t0 >= S) return;
     const int P = p.prefix_lens[r];
     const int L = P + S;
@@ -208,7 +226,7 @@ __global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_page
     row_valid = t < S;
     qrow = ((size_t)(q0 + (row_valid ? t : 0)) * p.num_q_heads + h) * D;
     qpos = row_valid ? P + t : L - 1;
-    const int kv_end = P + min(S, t0 + p.span);              // keys the tile needs
+    const int kv_end = P + min(S, t0 + span);                // keys the tile needs
     j0 = 0;
     n_steps = (kv_end + kBN - 1) / kBN;
     n_blk = (L + kBlock - 1) / kBlock;
@@ -530,9 +548,31 @@ __global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_page
   }
 }
 
-template <int D>
+template <int D, bool kStacked, bool kSplit>
+__global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_paged_attn_kernel(Params p) {
+  __shared__ Lds<D> sm_all[kSplit ? 2 : 1];
+  attn_tile<D, kStacked, kSplit, false>(p, sm_all, blockIdx.x);
+}
+
+// kTail: ping-pong tiles below pp_grid; the tail of the launch (at most half
+// a round of ping-pong tiles) runs as twice as many half tiles on the split
+// path, which fills the last round's idle CUs.  LDS: the split path's two
+// halves; a ping-pong tile uses the first.  Launches without a tail take the
+// plain kernel (one LDS half).  The ping-pong body stays in the kernel
+// itself: moved into a device function, it compiled to more registers and
+// ran 3-5% slower.
+template <int D, bool kTail>
 __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Params p) {
-  __shared__ Lds<D> sm;
+  static_assert(kPPThreads == 2 * kThreads, "the split tail runs 8 waves too");
+  __shared__ Lds<D> sm_all[kTail ? 2 : 1];
+  Lds<D>& sm = sm_all[0];
+  const int wg = blockIdx.x;
+  if constexpr (kTail) {
+    if (wg >= p.pp_grid) {
+      attn_tile<D, false, true, true>(p, sm_all, wg);
+      return;
+    }
+  }
   constexpr int kStride = Lds<D>::kStride;
   constexpr int vStride = Lds<D>::vStride;
   constexpr int KS = D / 16;     // MFMA k-steps over the head dim
@@ -548,7 +588,6 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
   const bool group_b = __builtin_amdgcn_readfirstlane(wave) >= 4;
 
   // ---- work tile (same order as the four-wave kernel) -----------------
-  const int wg = blockIdx.x;
   const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
   const int g = wg % p.num_kv_heads;
   const int sub = wg / p.num_kv_heads;
@@ -819,12 +858,29 @@ AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv
   const int group = num_q_heads / num_kv_heads;
   geo.heads_per_wg = (group % 4 == 0) ? 4 : (group % 2 == 0) ? 2 : 1;
   geo.head_tiles = num_q_heads / geo.heads_per_wg;
-  for (const int waves : {kPPWaves, kWaves}) {
-    geo.waves = waves;
-    geo.span = kNQ * (waves / geo.heads_per_wg);
+  // ping-pong tiles of 256 rows
+  geo.waves = kPPWaves;
+  geo.span = kNQ * (kPPWaves / geo.heads_per_wg);
+  geo.token_tiles = (max_q_len + geo.span - 1) / geo.span;
+  const long long tiles = (long long)geo.token_tiles * batch * geo.head_tiles;
+  geo.grid = geo.pp_grid = tiles;
+  if (tiles < kCUs) {
+    // less than a round: 128-row split tiles on twice as many work-groups
+    // (measured faster than the ping-pong tiles up to a full round)
+    geo.waves = kWaves;
+    geo.span = kNQ * (kWaves / geo.heads_per_wg);
     geo.token_tiles = (max_q_len + geo.span - 1) / geo.span;
     geo.grid = (long long)geo.token_tiles * batch * geo.head_tiles;
-    if (waves == kPPWaves && geo.grid >= kPPMinGrid) break;
+    geo.pp_grid = 0;
+    return geo;
+  }
+  // a last round at most half full runs as split half tiles (whose pairs
+  // must stay num_kv_heads work-groups apart, so the rounds must hold whole
+  // groups of KV heads)
+  const long long tail = tiles % kCUs;
+  if (tiles > kCUs && tail <= kCUs / 2 && kCUs % num_kv_heads == 0) {
+    geo.pp_grid = tiles - tail;
+    geo.grid = geo.pp_grid + 2 * tail;
   }
   return geo;
 }
@@ -849,12 +905,20 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
   p.token_tiles = geo.token_tiles;
   p.head_tiles = geo.head_tiles;
   p.scale_log2 = a.scale * kLog2e;
+  p.pp_grid = geo.pp_grid;
   const dim3 grid((unsigned)geo.grid);
   if (geo.waves == kPPWaves) {
+    const bool tail = geo.grid > geo.pp_grid;
     if (a.head_dim == 128) {
-      hipLaunchKernelGGL(prefill_paged_attn_pp_kernel<128>, grid, dim3(kPPThreads), 0, stream, p);
+      if (tail) {
+        hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<128, true>), grid, dim3(kPPThreads), 0, stream, p);
+      } else {
+        hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<128, false>), grid, dim3(kPPThreads), 0, stream, p);
+      }
+    } else if (tail) {
+      hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<64, true>), grid, dim3(kPPThreads), 0, stream, p);
     } else {
-      hipLaunchKernelGGL(prefill_paged_attn_pp_kernel<64>, grid, dim3(kPPThreads), 0, stream, p);
+      hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<64, false>), grid, dim3(kPPThreads), 0, stream, p);
     }
   } else if (a.head_dim == 128) {
     // fewer than one ping-pong work-group per CU: 128-row tiles, each run

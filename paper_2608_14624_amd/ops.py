@@ -28,7 +28,7 @@ EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_kv_write", "cs_kv_off
             "cs_scout_score_block", "cs_scout_select_victim", "cs_scout_predictability",
             "cs_scout_between_step", "cs_scout_state_bytes", "cs_scout_set_host_resident",
             "cs_scout_survival_all", "cs_scout_observe_touches", "cs_cascade_decode_attn",
-            "cs_cascade_decode_workspace_bytes")
+            "cs_cascade_decode_workspace_bytes", "cs_prefill_paged_attn_launch_shape")
 
 
 class ScoutParams(ctypes.Structure):
@@ -93,6 +93,9 @@ def _load():
         "cs_scout_set_host_resident": ([h, i32, i32], ctypes.c_int),
         "cs_scout_survival_all": ([h, ctypes.POINTER(f64)], ctypes.c_int),
         "cs_scout_observe_touches": ([h, vp, vp, vp, vp, i32], ctypes.c_int),
+        "cs_prefill_paged_attn_launch_shape": ([i32, i32, i32, i32, ctypes.POINTER(i32),
+                                                ctypes.POINTER(i64), ctypes.POINTER(i64)],
+                                               ctypes.c_int),
     }
     for name, (args, res) in sigs.items():
         fn = getattr(lib, name)
@@ -155,6 +158,19 @@ def cs_kv_prefetch_raw(host_k, host_v, dst_block_ids, n, k_pool, v_pool, num_blo
 def _require(cond, msg):
     if not cond:
         raise CacheScoutError(CS_ERR_INVALID_ARG, msg)
+
+
+ATTN_SPLIT, ATTN_PING_PONG = 0, 1
+
+
+def prefill_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads):
+    """``(kernel, grid, tail_work_groups)`` of a cs_prefill_paged_attn call
+    (host-only): kernel is ATTN_SPLIT or ATTN_PING_PONG."""
+    kernel, grid, tail = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64()
+    _check(_lib.cs_prefill_paged_attn_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads,
+                                                   ctypes.byref(kernel), ctypes.byref(grid),
+                                                   ctypes.byref(tail)))
+    return kernel.value, grid.value, tail.value
 
 
 def cs_prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out, *,

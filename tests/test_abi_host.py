@@ -245,3 +245,32 @@ def test_library_exports_only_the_declared_calls():
     text_symbols = sorted(line.split()[-1] for line in out.splitlines()
                           if len(line.split()) == 3 and line.split()[1] == "T")
     assert text_symbols == declared_functions()
+
+
+@pytest.mark.parametrize("batch,max_q,hq,hkv,expect", [
+    # 256-row ping-pong tiles: T = ceil(max_q / span) * batch * head_tiles,
+    # span = 32 * 8 / heads_per_wg, head_tiles = hq / heads_per_wg
+    (1, 1024, 32, 8, (ops.ATTN_SPLIT, 32 * 8, 0)),          # T = 128: split 128-row tiles
+    (1, 1984, 32, 8, (ops.ATTN_SPLIT, 62 * 8, 0)),          # T = 248: split
+    (1, 1985, 32, 8, (ops.ATTN_PING_PONG, 256, 0)),         # T = 256: one full round
+    (1, 2049, 32, 8, (ops.ATTN_PING_PONG, 256 + 2 * 8, 16)),    # T = 264: tail of 8 tiles
+    (2, 1024, 32, 8, (ops.ATTN_PING_PONG, 256, 0)),         # one full round
+    (5, 500, 32, 8, (ops.ATTN_PING_PONG, 256 + 2 * 64, 128)),   # T = 320: tail of 64 tiles
+    (3, 1024, 32, 8, (ops.ATTN_PING_PONG, 256 + 2 * 128, 256)),  # T = 384: tail of 128
+    (7, 512, 32, 8, (ops.ATTN_PING_PONG, 448, 0)),          # T = 448: tail over half a round
+    (7, 640, 16, 8, (ops.ATTN_PING_PONG, 256 + 2 * 24, 48)),    # G = 2: span 128, T = 280
+    (17, 512, 8, 8, (ops.ATTN_PING_PONG, 256 + 2 * 16, 32)),    # G = 1: span 256, T = 272
+    (11, 512, 12, 3, (ops.ATTN_PING_PONG, 11 * 2 * 12, 0)),     # 3 KV heads: no tail
+    (0, 512, 32, 8, (ops.ATTN_SPLIT, 0, 0)),
+    (4, 0, 32, 8, (ops.ATTN_SPLIT, 0, 0)),
+])
+def test_prefill_launch_shape(batch, max_q, hq, hkv, expect):
+    assert ops.prefill_launch_shape(batch, max_q, hq, hkv) == expect
+
+
+@pytest.mark.parametrize("args", [(-1, 64, 8, 2), (1, -1, 8, 2), (1, 64, 0, 2), (1, 64, 8, 3),
+                                  (1, 64, 8, 0)])
+def test_prefill_launch_shape_rejects_bad_arguments(args):
+    with pytest.raises(ops.CacheScoutError) as ei:
+        ops.prefill_launch_shape(*args)
+    assert ei.value.args[0].startswith("CS_ERR_INVALID_ARG")

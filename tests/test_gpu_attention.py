@@ -92,6 +92,29 @@ def test_edge_cases_full(P, name):
     check_full(P, wl)
 
 
+TAIL = {
+    # ping-pong launches whose last round is at most half full: that round's
+    # tiles run as split 128-row halves in the same launch
+    "tail_g4": ([300, 40], [Invocation(0, 500), Invocation(1, 130), Invocation(0, 449),
+                            Invocation(1, 64), Invocation(0, 1)], 32, 8, 128),
+    "tail_g2_d64": ([90, 17], [Invocation(i % 2, n) for i, n in
+                               enumerate([640, 600, 1, 129, 300, 0, 77])], 16, 8, 64),
+    "tail_g1": ([200], [Invocation(0, 512 - 29 * i) for i in range(17)], 8, 8, 128),
+}
+
+
+@pytest.mark.parametrize("name", sorted(TAIL))
+def test_ping_pong_launch_with_split_tail(P, name):
+    ops, _ = P
+    anchors, invs, hq, hkv, d = TAIL[name]
+    wl = build_workload(name, 99, anchors, invs, num_q_heads=hq, num_kv_heads=hkv,
+                        head_dim=d, num_blocks=512)
+    kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, hq, hkv)
+    print(f"[case] {name}: grid={grid} tail work-groups={tail}", flush=True)
+    assert kernel == ops.ATTN_PING_PONG and tail > 0
+    check_full(P, wl)
+
+
 def test_agent_batch_sampled(P):
     _, pipeline = P
     wl = make_config("agent_batch")
