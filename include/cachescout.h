@@ -173,7 +173,7 @@ int cs_prefill_paged_attn_launch_shape(int32_t batch, int32_t max_q_len, int32_t
  *                  [n][num_kv_heads][block_size][head_dim], 16-byte aligned.
  *                  Anything else -> CS_ERR_INVALID_ARG.
  *   dst_block_ids  device, int32 [n]; unique, each in [0, num_blocks).
- *   n              number of blocks, at most min(num_blocks, 2^30); 0 is a
+ *   n              number of blocks, at most min(num_blocks, 2^30 - 1); 0 is a
  *                  no-op returning CS_OK.
  *   k_pool, v_pool device, as in cs_prefill_paged_attn, 16-byte aligned.
  *   num_blocks, num_kv_heads, head_dim (64 or 128), block_size (16).
@@ -316,7 +316,7 @@ int cs_kv_write(const void *k_new, const void *v_new, const int32_t *slot_mappin
  *                  [n][num_kv_heads][block_size][head_dim], 16-byte aligned;
  *                  anything else -> CS_ERR_INVALID_ARG.  Read them only after
  *                  the stream has passed this call.
- *   n <= 2^30; n == 0 is a no-op returning CS_OK.
+ *   n <= 2^30 - 1; n == 0 is a no-op returning CS_OK.
  */
 int cs_kv_offload(const int32_t *src_block_ids, int32_t n, const void *k_pool,
                   const void *v_pool, int32_t num_blocks, void *host_k_blocks,

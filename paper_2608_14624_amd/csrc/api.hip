@@ -43,8 +43,8 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(CS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
-// the block copies index K and V units of a call with 32-bit ints
-constexpr int32_t kMaxCopyBlocks = 1 << 30;
+// the block copies index the K and V units of a call (2 n) with 32-bit ints
+constexpr int32_t kMaxCopyBlocks = (1 << 30) - 1;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -342,7 +342,7 @@ int cs_kv_prefetch(const void* host_k_blocks, const void* host_v_blocks,
                    int32_t num_blocks, int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                    cs_stream_t stream) {
   if (n < 0 || num_blocks < 0) return fail(CS_ERR_INVALID_ARG, "negative size argument");
-  if (n > kMaxCopyBlocks) return fail(CS_ERR_INVALID_ARG, "n = %d exceeds 2^30 blocks", n);
+  if (n > kMaxCopyBlocks) return fail(CS_ERR_INVALID_ARG, "n = %d exceeds 2^30 - 1 blocks", n);
   if (num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
     return fail(CS_ERR_INVALID_ARG, "num_kv_heads, head_dim and block_size must be positive");
   if (head_dim != 64 && head_dim != 128)
@@ -542,7 +542,7 @@ int cs_kv_offload(const int32_t* src_block_ids, int32_t n, const void* k_pool, c
                   int32_t num_blocks, void* host_k_blocks, void* host_v_blocks,
                   int32_t num_kv_heads, int32_t head_dim, int32_t block_size, cs_stream_t stream) {
   if (n < 0 || num_blocks < 0) return fail(CS_ERR_INVALID_ARG, "negative size argument");
-  if (n > kMaxCopyBlocks) return fail(CS_ERR_INVALID_ARG, "n = %d exceeds 2^30 blocks", n);
+  if (n > kMaxCopyBlocks) return fail(CS_ERR_INVALID_ARG, "n = %d exceeds 2^30 - 1 blocks", n);
   if (num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
     return fail(CS_ERR_INVALID_ARG, "num_kv_heads, head_dim and block_size must be positive");
   if (head_dim != 64 && head_dim != 128)

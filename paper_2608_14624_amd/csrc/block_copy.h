@@ -66,4 +66,37 @@ __device__ __forceinline__ void copy_units(int units, long long vecs, SrcOf src_
   }
 }
 
+// Lean variant for a copy that runs beside attention: at most kLeanVgprs
+// registers per lane (two 16-byte vectors in flight), so its waves fit in the
+// registers an attention work-group leaves free on a CU (two waves of at most
+// 248 VGPRs per SIMD) and run on the same CUs instead of taking CUs of their
+// own.  kLeanGroups work-groups keep 128 KiB in flight, which still fills the
+// host link (52 GB/s measured): more (64 work-groups, 512 KiB) slowed the
+// attention running beside the copy by 14% instead of 9%, fewer (8) left
+// the link at 41 GB/s.
+constexpr int kLeanGroups = 16;
+constexpr int kLeanVgprs = 16;
+
+inline unsigned lean_copy_grid(long long units) {
+  return (unsigned)(units < kLeanGroups ? units : kLeanGroups);
+}
+
+template <bool kNtLoad, bool kNtStore, class SrcOf, class DstOf>
+__device__ __forceinline__ void copy_units_lean(int units, int vecs, SrcOf src_of, DstOf dst_of) {
+  for (int u = blockIdx.x; u < units; u += gridDim.x) {
+    const u32x4* src = src_of(u);
+    u32x4* dst = dst_of(u);
+    for (int i = threadIdx.x; i < vecs; i += 2 * kCopyThreads) {
+      const int i1 = i + kCopyThreads;
+      const u32x4 a = kNtLoad ? __builtin_nontemporal_load(src + i) : src[i];
+      u32x4 b = a;
+      if (i1 < vecs) b = kNtLoad ? __builtin_nontemporal_load(src + i1) : src[i1];
+      if (kNtStore) __builtin_nontemporal_store(a, dst + i); else dst[i] = a;
+      if (i1 < vecs) {
+        if (kNtStore) __builtin_nontemporal_store(b, dst + i1); else dst[i1] = b;
+      }
+    }
+  }
+}
+
 }  // namespace cs

@@ -216,6 +216,18 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
       const int cc = lane + 64 * u;
       *reinterpret_cast<uint4*>(&sm.v[wave][(cc / kRowChunks) * vStride + (cc % kRowChunks) * 8]) = vreg[u];
     }
+    // rows past the end of the sequence (inside its last block) overwritten
+    // with zeros: their probabilities are 0, but 0 times a stale NaN or Inf
+    // in the pool is NaN
+    if ((ch + 1) * kChunk > end) {
+#pragma unroll
+      for (int u = 0; u < kVLoads; ++u) {
+        const int cc = lane + 64 * u;
+        if (ch * kChunk + cc / kRowChunks >= end)
+          *reinterpret_cast<uint4*>(&sm.v[wave][(cc / kRowChunks) * vStride + (cc % kRowChunks) * 8]) =
+              make_uint4(0, 0, 0, 0);
+      }
+    }
     // S^T = K Q^T: two 16-key tiles
     f32x4 s[2] = {f32x4{}, f32x4{}};
 #pragma unroll

@@ -23,9 +23,11 @@
 //     the PV product (V^T) comes from two transposing 8-byte LDS reads
 //     (ds_read_b64_tr_b16).  Rows are padded to spread LDS banks.  Block ids
 //     are read from the block table per 16-token block.
-//   * Masking is a select to -inf (never an additive mask), so positions past
-//     the end of a sequence inside its last block never contribute whatever
-//     they hold; whole blocks past the end are zero-filled in LDS, never read.
+//   * Masking is a select to -inf (never an additive mask), so K positions
+//     past the end of a sequence inside its last block never contribute
+//     whatever they hold; the V rows there are stored to LDS as zeros (their
+//     probabilities are 0, and 0 times a NaN would not be), and whole blocks
+//     past the end are zero-filled in LDS, never read.
 //   * Softmax runs in base 2 with log2(e) folded into the scale.
 //
 // Work-group order: the KV head varies fastest, so with 8 KV heads the 8 XCDs
@@ -189,6 +191,7 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
   int j0;               // first 64-key step
   int n_steps;          // steps of the work-group
   int n_blk;            // blocks of the key range reached through bt
+  int kv_len;           // keys of the sequence (V rows from there on are zeroed)
   int wave_qmin;        // first key position some row of this wave cannot see
   const int32_t* bt;
   int chunk = 0;
@@ -230,6 +233,7 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
     j0 = 0;
     n_steps = (kv_end + kBN - 1) / kBN;
     n_blk = (L + kBlock - 1) / kBlock;
+    kv_len = L;
     bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
     wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
   } else {
@@ -256,6 +260,7 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
     j0 = kb / kBN;
     n_steps = (ke - kb + kBN - 1) / kBN;
     n_blk = SH / kBlock;
+    kv_len = SH;                                              // whole blocks
     bt = p.block_tables + (size_t)s0 * p.max_blocks_per_seq;   // the group's shared blocks
     wave_qmin = ke - 1;
   }
@@ -326,6 +331,21 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
       *reinterpret_cast<uint4*>(&buf[key * stride + (c % kChunksPerRow) * 8]) = src[u];
     }
   };
+  // V rows past the end of the sequence inside its last block (key0: the
+  // block's first key) are overwritten with zeros after the block is
+  // stored: their probabilities are 0, but 0 times a stale NaN or Inf in the
+  // pool is NaN.  Only the one block that holds the end takes this path.
+  auto zero_tail = [&](uint16_t* buf, int key0) {
+    if (!kStacked && key0 < kv_len && key0 + kBlock > kv_len) {   // shared prefixes: whole blocks
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) {
+        const int c = lane + 64 * u;
+        if (key0 + c / kChunksPerRow >= kv_len)
+          *reinterpret_cast<uint4*>(&buf[(wave_u * kBlock + c / kChunksPerRow) * vStride +
+                                         (c % kChunksPerRow) * 8]) = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
   // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
   // transposing reads.  ds_read_b64_tr_b16 treats the 8-byte rows addressed
   // by the 16 lanes of a group as a 16 x 4 matrix M and hands lane j of the
@@ -371,6 +391,7 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
     load_tile(vreg[0], vbase, id0);
     store_tile(kreg[0], sm.k[0], kStride);
     store_tile(vreg[0], sm.v[0], vStride);
+    zero_tail(sm.v[0], j0 * kBN + wave_u * kBlock);
     if (n_steps > 1) {
       const int id1 = block_id(1);
       load_tile(kreg[1], kbase, id1);
@@ -394,6 +415,7 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
     if (j + 1 < n_steps) {
       store_tile(kst, sm.k[cur ^ 1], kStride);     // K_{j+1}, V_{j+1}
       store_tile(vst, sm.v[cur ^ 1], vStride);
+      zero_tail(sm.v[cur ^ 1], kstart + kBN + wave_u * kBlock);
     }
     if (j + 3 < n_steps) {                          // in flight for two steps
       load_tile(kst, kbase, id_next);
@@ -660,6 +682,21 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
       *reinterpret_cast<uint4*>(&dst[key * stride + (c % kChunksPerRow) * 8]) = src[u];
     }
   };
+  // V rows past the end of the sequence inside its last block (key0: the
+  // block's first key) are overwritten with zeros after the block is stored
+  // (probabilities 0 times a stale NaN or Inf would be NaN); only the block
+  // that holds the end takes this path.
+  auto zero_tail = [&](uint16_t* dst, int key0) __attribute__((always_inline)) {
+    if (key0 < L && key0 + kBlock > L) {
+#pragma unroll
+      for (int u = 0; u < kKLoads; ++u) {
+        const int c = lane + 64 * u;
+        if (key0 + c / kChunksPerRow >= L)
+          *reinterpret_cast<uint4*>(&dst[(slot_u * kBlock + c / kChunksPerRow) * vStride +
+                                         (c % kChunksPerRow) * 8]) = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
   // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
   // transposing reads (ds_read_b64_tr_b16: lane j of a 16-lane group gets
   // M[4e + j/4][j%4] of the 8-byte rows its lanes address).
@@ -803,7 +840,10 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
         if (j + 1 < n_steps) store_tile(st, sm.k[(j + 1) & 1], kStride);
         if (j + 3 < n_steps) load_tile(st, block_id(j + 3));
       } else {
-        if (j < n_steps) store_tile(st, sm.v[j & 1], vStride);
+        if (j < n_steps) {
+          store_tile(st, sm.v[j & 1], vStride);
+          zero_tail(sm.v[j & 1], j * kBN + slot_u * kBlock);
+        }
         if (j + 2 < n_steps) load_tile(st, block_id(j + 2));
       }
       __builtin_amdgcn_sched_barrier(0);

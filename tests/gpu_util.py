@@ -53,3 +53,29 @@ def compare_rows(wl, got_bits, samples, k_pool=None, v_pool=None):
     assert np.isfinite(got).all(), "non-finite output"
     err = np.abs(got - ref)
     return float(err.max()), float(err.mean())
+
+
+BF16_QNAN, BF16_POS_INF = 0x7FC0, 0x7F80
+
+
+def poison_tails(wl, bits=(BF16_QNAN, BF16_POS_INF)):
+    """Fill the pool positions past the end of every sequence's last block
+    (K and V, all heads) with NaN and Inf, alternating by position, where no
+    sequence reads them as keys.  Returns the number of positions poisoned."""
+    kv = wl.prefix_lens.astype(np.int64) + wl.q_lens.astype(np.int64)
+    bs = wl.block_size
+    # first position of each slot that some sequence reads as a key
+    limit = {}
+    for r in range(wl.batch):
+        L = int(kv[r])
+        for b in range(-(-L // bs)):
+            slot = int(wl.block_tables[r, b])
+            limit[slot] = max(limit.get(slot, 0), min(bs, L - b * bs))
+    n = 0
+    for slot, used in limit.items():
+        for pos in range(used, bs):
+            v = np.uint16(bits[pos % len(bits)])
+            wl.k_pool[slot, :, pos, :] = v
+            wl.v_pool[slot, :, pos, :] = v
+            n += 1
+    return n

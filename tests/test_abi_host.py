@@ -105,7 +105,7 @@ def prefetch(**kw):
     (dict(dst_block_ids=None), ops.CS_ERR_INVALID_ARG),
     (dict(n=65), ops.CS_ERR_INVALID_ARG),
     (dict(host_v=FAKE + 4), ops.CS_ERR_INVALID_ARG),
-    (dict(n=2 ** 30 + 1, num_blocks=2 ** 31 - 1), ops.CS_ERR_INVALID_ARG),
+    (dict(n=2 ** 30, num_blocks=2 ** 31 - 1), ops.CS_ERR_INVALID_ARG),   # 2 n units overflow int32
 ])
 def test_prefetch_rejects_bad_arguments(kw, status):
     assert prefetch(**kw) == status
@@ -149,7 +149,7 @@ OGOOD = dict(src_block_ids=FAKE, n=4, k_pool=FAKE, v_pool=FAKE, num_blocks=64, h
     (dict(host_k=None), ops.CS_ERR_INVALID_ARG),
     (dict(src_block_ids=None), ops.CS_ERR_INVALID_ARG),
     (dict(host_v=FAKE + 4), ops.CS_ERR_INVALID_ARG),
-    (dict(n=2 ** 30 + 1), ops.CS_ERR_INVALID_ARG),
+    (dict(n=2 ** 30), ops.CS_ERR_INVALID_ARG),
 ])
 def test_kv_offload_rejects_bad_arguments(kw, status):
     args = dict(OGOOD)

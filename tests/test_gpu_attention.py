@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import MAX_ABS, MEAN_ABS, compare_full, compare_rows, sample_rows
+from gpu_util import MAX_ABS, MEAN_ABS, compare_full, compare_rows, poison_tails, sample_rows
 from paper_2608_14624_amd.workload import Invocation, build_workload, make_config
 
 pytestmark = pytest.mark.gpu
@@ -112,6 +112,27 @@ def test_ping_pong_launch_with_split_tail(P, name):
     kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, hq, hkv)
     print(f"[case] {name}: grid={grid} tail work-groups={tail}", flush=True)
     assert kernel == ops.ATTN_PING_PONG and tail > 0
+    check_full(P, wl)
+
+
+@pytest.mark.parametrize("shape", ["split", "ping_pong", "ping_pong_tail"])
+def test_nan_and_inf_past_the_end_do_not_leak(P, shape):
+    """Pool positions past a sequence's end inside its last block may hold
+    anything (a recycled slot): NaN and Inf there must not reach the output,
+    on every kernel path."""
+    ops, _ = P
+    invs = {"split": [Invocation(0, 37), Invocation(1, 90), Invocation(0, 5)],
+            "ping_pong": [Invocation(i % 2, 1000 + 13 * i) for i in range(2)],
+            "ping_pong_tail": [Invocation(i % 2, 450 + 7 * i) for i in range(5)]}[shape]
+    wl = build_workload("nan_tail", 5, [61, 200], invs, num_q_heads=32, num_kv_heads=8,
+                        head_dim=128, num_blocks=512)
+    kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, 32, 8)
+    assert (kernel, tail > 0) == {"split": (ops.ATTN_SPLIT, False),
+                                  "ping_pong": (ops.ATTN_PING_PONG, False),
+                                  "ping_pong_tail": (ops.ATTN_PING_PONG, True)}[shape]
+    n = poison_tails(wl)
+    print(f"[case] nan tails, {shape}: {n} poisoned positions, grid={grid}", flush=True)
+    assert n > 0
     check_full(P, wl)
 
 

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import MAX_ABS, MEAN_ABS
+from gpu_util import MAX_ABS, MEAN_ABS, poison_tails
 from paper_2608_14624_amd.workload import Invocation, build_workload, decode_view, make_config
 
 pytestmark = pytest.mark.gpu
@@ -253,3 +253,20 @@ def test_cascade_workspace_reuse_and_debug_checks(monkeypatch):
     with pytest.raises(ops.CacheScoutError, match="max_rest_len"):
         run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"], cv["max_group_seqs"],
                     cv["max_shared_len"], workspace=ws, max_rest_len=cv["max_rest_len"] - 1)
+
+
+def test_decode_and_cascade_ignore_nan_and_inf_past_the_end():
+    """NaN and Inf in the pool positions past each sequence's end (inside its
+    last block) must not reach the decode or cascade output."""
+    invs = [Invocation(0, 3, True), Invocation(1, 40, True), Invocation(0, 17, True),
+            Invocation(1, 1, True), Invocation(2, 9, False)]
+    wl = build_workload("nan_tail_dec", 43, [700, 530, 90], invs, num_q_heads=32, num_kv_heads=8,
+                        head_dim=128, num_blocks=1024)
+    n = poison_tails(wl)
+    print(f"[case] decode/cascade nan tails: {n} poisoned positions", flush=True)
+    assert n > 0
+    check(run_decode(wl), oracle_last_rows(wl), "decode vs oracle")
+    q, seq_lens, bt, cv = grouped_batch(wl)
+    got = run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"],
+                      cv["max_group_seqs"], cv["max_shared_len"])
+    check(got, oracle_decode(q, seq_lens, bt, wl), "cascade vs oracle")

@@ -13,6 +13,8 @@
   P + 1 keys with no mask.
 * Closed forms: zero queries give the running mean of the values; constant
   values give that constant; one dominant key gives its value.
+* Pool positions no sequence reaches as a key (past the end of its last
+  block, unused slots) are never read: NaN and Inf there change nothing.
 """
 
 import numpy as np
@@ -60,6 +62,28 @@ def test_invariant1_block_placement_is_irrelevant_bitwise():
     v2[perm] = wl.v_pool
     bt2 = perm[wl.block_tables].astype(np.int32)
     moved = run_oracle(wl, k_pool=k2, v_pool=v2, block_tables=bt2)
+    assert np.array_equal(base.view(np.uint64), moved.view(np.uint64))
+
+
+def test_positions_past_the_end_are_never_read():
+    """Pool positions past each sequence's end (inside its last block, and
+    every slot no table reaches) may hold anything: filled with NaN and Inf,
+    the output is bitwise unchanged and finite."""
+    wl = small_batch()
+    base = run_oracle(wl)
+    k2, v2 = wl.k_pool.copy(), wl.v_pool.copy()
+    kv = wl.prefix_lens.astype(np.int64) + wl.q_lens.astype(np.int64)
+    used = np.zeros((wl.num_blocks, wl.block_size), dtype=bool)
+    for r in range(wl.batch):
+        for j in range(int(kv[r])):
+            used[wl.block_tables[r, j // wl.block_size], j % wl.block_size] = True
+    poison = np.where(np.arange(wl.block_size) % 2 == 0, 0x7FC0, 0x7F80).astype(np.uint16)
+    for slot, pos in zip(*np.nonzero(~used)):
+        k2[slot, :, pos, :] = poison[pos]
+        v2[slot, :, pos, :] = poison[pos]
+    assert (~used).sum() > 0
+    moved = run_oracle(wl, k_pool=k2, v_pool=v2)
+    assert np.isfinite(moved).all()
     assert np.array_equal(base.view(np.uint64), moved.view(np.uint64))
 
 
