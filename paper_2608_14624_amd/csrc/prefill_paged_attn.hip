@@ -665,9 +665,8 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
   };
   using Stage = uint4[kKLoads];
   uint4 stage[2][kKLoads];
-  auto load_tile = [&](Stage& dst, int id) __attribute__((always_inline)) {
+  auto load_tile_at = [&](Stage& dst, const uint16_t* src, int id) __attribute__((always_inline)) {
     if (id >= 0) {
-      const uint16_t* src = my_base + (size_t)id * slot_elems;
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) {
         const int c = lane + 64 * u;
@@ -677,6 +676,9 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
 #pragma unroll
       for (int u = 0; u < kKLoads; ++u) dst[u] = make_uint4(0, 0, 0, 0);
     }
+  };
+  auto load_tile = [&](Stage& dst, int id) __attribute__((always_inline)) {
+    load_tile_at(dst, my_base + (size_t)(id >= 0 ? id : 0) * slot_elems, id);
   };
   auto store_tile = [&](const Stage& src, uint16_t* dst, int stride) __attribute__((always_inline)) {
 #pragma unroll
@@ -824,14 +826,17 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
     // ---- prologue ------------------------------------------------------
     // K waves: K_0 into LDS, K_1 and K_2 in registers; V waves: V_0 and V_1
     // in registers (V_j is stored at iteration j, K_{j+1} at iteration j).
+    int id_next;     // block of the step the next iteration loads, read ahead
     if (!kB) {
       load_tile(stage[0], block_id(0));
       store_tile(stage[0], sm.k[0], kStride);
       load_tile(stage[1], block_id(1));
       load_tile(stage[0], block_id(2));
+      id_next = block_id(3);
     } else {
       load_tile(stage[0], block_id(0));
       load_tile(stage[1], block_id(1));
+      id_next = block_id(2);
     }
 
     // One iteration: stage data for the next iteration, then the two phases in
@@ -840,15 +845,20 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
     // read in iteration j-1, before this iteration's barrier.
     auto iteration = [&](const int j, Stage& st) __attribute__((always_inline)) {
       __syncthreads();
+      // the scalar read of the block id is waited for here, before this
+      // iteration's LDS stores, so the wait does not include them
+      const int id = id_next;
+      const uint16_t* src = my_base + (size_t)(id >= 0 ? id : 0) * slot_elems;
+      __builtin_amdgcn_sched_barrier(0);
       if (!kB) {
         if (j + 1 < n_steps) store_tile(st, sm.k[(j + 1) & 1], kStride);
-        if (j + 3 < n_steps) load_tile(st, block_id(j + 3));
+        if (j + 3 < n_steps) load_tile_at(st, src, id);
       } else {
         if (j < n_steps) {
           store_tile(st, sm.v[j & 1], vStride);
           zero_tail(sm.v[j & 1], j * kBN + slot_u * kBlock);
         }
-        if (j + 2 < n_steps) load_tile(st, block_id(j + 2));
+        if (j + 2 < n_steps) load_tile_at(st, src, id);
       }
       __builtin_amdgcn_sched_barrier(0);
       if (!kB) {
@@ -860,6 +870,10 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
         __builtin_amdgcn_sched_barrier(0);
         mfma_phase(j);
       }
+      // the next iteration's block id, read once this iteration's LDS reads
+      // have been consumed
+      __builtin_amdgcn_sched_barrier(0);
+      id_next = block_id(kB ? j + 3 : j + 4);
     };
     // register stage of iteration j: K waves stage[(j+1)&1] (K_{j+1} is
     // stored, K_{j+3} loaded), V waves stage[j&1] (V_j stored, V_{j+2} loaded);
