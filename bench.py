@@ -50,6 +50,10 @@ DESCRIPTIONS = {
     "decode_batch": "128 sequences over 8 agents, anchors U[4096,8192] + lognormal history "
                     "(median 512) in [128,4096], one token decoded per sequence, 32 query / 8 "
                     "KV heads, head_dim 128",
+    "llama70b_prefetch_tp8": "one GPU's shard of llama70b_prefetch split 8 ways by KV head: "
+                             "the same 16 invocations and prefetches with 8 query / 1 KV head",
+    "agent_batch_tp8": "one GPU's shard of agent_batch split 8 ways by KV head: the same 32 "
+                       "invocations with 4 query / 1 KV head",
 }
 
 
@@ -114,7 +118,7 @@ def cpu_baseline(wl, budget_s=20.0):
         if elapsed >= budget_s:
             break
     return {"value": done_flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "host": host_description(),
             "sample": f"{n_inv} of {wl.batch} invocations of {wl.name}, full float64 "
                       f"oracle ({elapsed:.1f} s)"}
 
@@ -133,7 +137,39 @@ def _time_launches(fn, steps, warmup, stream):
         e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    return wall, sum(e0.elapsed_time(e1) for e0, e1 in evs) / steps
+    ms = [e0.elapsed_time(e1) for e0, e1 in evs]
+    return wall, sum(ms) / steps, ms
+
+
+def percentiles_us(ms_list):
+    """Median, p10 and p90 of launch durations given in milliseconds, in us."""
+    import numpy as np
+    a = np.asarray(ms_list, dtype=np.float64) * 1e3
+    return {"p10_us": round(float(np.percentile(a, 10)), 2),
+            "median_us": round(float(np.percentile(a, 50)), 2),
+            "p90_us": round(float(np.percentile(a, 90)), 2)}
+
+
+def host_description():
+    """CPU model and BLAS library of the host the oracle runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
+    except Exception:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "blas": blas, "logical_cpus": os.cpu_count()}
 
 
 def bench_copy(args, dev):
@@ -209,6 +245,41 @@ def bench_copy(args, dev):
         def fn():
             ops.cs_kv_write(k_new, v_new, slots, k_pool, v_pool, stream=stream)
         peak, bound, unit_desc = PEAK_HBM_GBS, "hbm", f"{t} tokens"
+    elif args.component == "kv_prefetch":
+        # the prefetch alone: 256 blocks (16 MiB) is the line's value; the
+        # sweep and a plain pinned host-to-device copy of the same bytes (the
+        # link as the runtime's own copy reaches it) go beside it
+        sweep, n_main = {}, 256
+        g = torch.Generator().manual_seed(7)
+        for n in (64, 256, 1024, 4096):
+            ids_n = torch.from_numpy(np.random.default_rng(n).choice(wl.num_blocks, n, replace=False)
+                                     .astype(np.int32)).to(dev)
+            hk = torch.empty((n, hkv, 16, d), dtype=torch.bfloat16, pin_memory=True)
+            hv = torch.empty_like(hk, pin_memory=True)
+            hk.copy_(torch.randn(hk.shape, generator=g).to(torch.bfloat16))
+            hv.copy_(torch.randn(hv.shape, generator=g).to(torch.bfloat16))
+            nbytes = 2 * n * hkv * 16 * d * 2
+
+            def pf(hk=hk, hv=hv, ids_n=ids_n):
+                ops.cs_kv_prefetch(hk, hv, ids_n, k_pool, v_pool, stream=stream)
+            _, ms, _ = _time_launches(pf, max(5, args.steps // 5), 2, stream)
+            sweep[str(n)] = {"bytes": nbytes, "avg_launch_us": round(ms * 1e3, 2),
+                             "gbs": round(nbytes / (ms * 1e-3) / 1e9, 2)}
+            if n == n_main:
+                host_k, host_v, ids, moved = hk, hv, ids_n, nbytes
+        flat = host_k.view(-1)
+        dev_buf = torch.empty(flat.shape, dtype=flat.dtype, device=dev)
+
+        def h2d():
+            dev_buf.copy_(flat, non_blocking=True)
+        _, ms, _ = _time_launches(h2d, 20, 3, stream)
+        memcpy = {"bytes": flat.numel() * 2, "gbs": round(flat.numel() * 2 / (ms * 1e-3) / 1e9, 2),
+                  "note": "torch copy_ from the pinned K buffer: the runtime's own host-to-"
+                          "device copy, a measured reference for the link"}
+
+        def fn():
+            ops.cs_kv_prefetch(host_k, host_v, ids, k_pool, v_pool, stream=stream)
+        peak, bound, unit_desc = PEAK_PCIE5_X16_GBS, "host_link", f"{n_main} blocks"
     else:
         n = 256
         ids = torch.from_numpy(np.random.default_rng(5).choice(wl.num_blocks, n, replace=False)
@@ -230,11 +301,15 @@ def bench_copy(args, dev):
         "kv_write": ("kv_write_kernel", ("paper_2608_14624_amd/csrc/kv_copy.hip",)),
         "kv_offload": ("kv_offload_kernel", ("paper_2608_14624_amd/csrc/kv_copy.hip",
                                              "paper_2608_14624_amd/csrc/block_copy.h")),
+        "kv_prefetch": ("kv_prefetch_kernel", ("paper_2608_14624_amd/csrc/kv_prefetch.hip",
+                                               "paper_2608_14624_amd/csrc/block_copy.h")),
     }[args.component]
     traffic = load_traffic(kernel, args.workload, source_hash(sources))
-    wall, avg_ms = _time_launches(fn, args.steps, args.warmup, stream)
+    wall, avg_ms, all_ms = _time_launches(fn, args.steps, args.warmup, stream)
     gbs = moved / (avg_ms * 1e-3) / 1e9
     extra = {}
+    if args.component == "kv_prefetch":
+        extra = {"sweep_blocks": sweep, "memcpy_h2d": memcpy}
     if args.component in ("decode", "cascade_decode"):
         extra = {"logical_bytes": logical,
                  "logical_rate_gbs": round(logical / (avg_ms * 1e-3) / 1e9, 2),
@@ -248,7 +323,8 @@ def bench_copy(args, dev):
                        "bytes_per_launch": moved},
             "roofline": {"bound": bound, "achieved": round(gbs, 2), "peak": peak, "unit": "GB/s",
                          "frac": round(gbs / peak, 4), "traffic": traffic, "kernel": kernel,
-                         "avg_launch_us": round(avg_ms * 1e3, 2), **extra},
+                         "avg_launch_us": round(avg_ms * 1e3, 2),
+                         "launch_us": percentiles_us(all_ms), **extra},
             "cpu_baseline": None}
 
 
@@ -351,10 +427,11 @@ def main():
                          "control plane's between-step decision (cs_scout_*); the warmup "
                          "steps let it learn the dispatch cycle")
     ap.add_argument("--component", default="pipeline",
-                    choices=("pipeline", "kv_write", "kv_offload", "decode", "cascade_decode",
-                             "control_plane"),
-                    help="pipeline (default): the serving step; kv_write / kv_offload: "
-                         "the write-back scatter and the offload copy on their own; "
+                    choices=("pipeline", "kv_write", "kv_offload", "kv_prefetch", "decode",
+                             "cascade_decode", "control_plane"),
+                    help="pipeline (default): the serving step; kv_write / kv_offload / "
+                         "kv_prefetch: the write-back scatter, the offload copy and the "
+                         "prefetch (with a sweep over 64-4096 blocks) on their own; "
                          "decode / cascade_decode: paged decode attention, per sequence or "
                          "with each agent's anchor read once (use --workload decode_batch); "
                          "control_plane: the host-side scout on a synthetic agent trace")
@@ -466,15 +543,42 @@ def main():
         iso = sum(e0.elapsed_time(e1) for e0, e1 in iso_ms) / len(iso_ms)
         iso_gbs = pf_bytes_per_step / n_launch / (iso * 1e-3) / 1e9
         pf_gbs = pf_bytes_per_step * args.steps / (sum(pf_ms) * 1e-3) / 1e9
+        # the attention launches of a step alone, back to back on one stream
+        # (all of their work, no copy beside them): how much the prefetch
+        # running beside them costs, and the serial sum the overlap beats
+        def attention_only():
+            for b in pipe.batches:
+                b.attention(stream=main_stream)
+        for _ in range(args.warmup):
+            attention_only()
+        torch.cuda.synchronize()
+        al_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(n_launch)] for _ in range(args.steps)]
+        for row in al_ev:
+            for b, (e0, e1) in zip(pipe.batches, row):
+                e0.record(main_stream)
+                b.attention(stream=main_stream)
+                e1.record(main_stream)
+        torch.cuda.synchronize()
+        alone_ms = [e0.elapsed_time(e1) for row in al_ev for e0, e1 in row]
+        alone_step_ms = sum(alone_ms) / args.steps
         prefetch = {"value": round(pf_gbs, 2), "unit": "GB/s",
                     "frac_link": round(pf_gbs / PEAK_PCIE5_X16_GBS, 4),
                     "link_peak": PEAK_PCIE5_X16_GBS, "frac_hbm": round(pf_gbs / PEAK_HBM_GBS, 5),
                     "bytes_per_step": pf_bytes_per_step, "launches_per_step": n_launch,
                     "avg_launch_us": round(sum(pf_ms) / len(pf_ms) * 1e3, 2),
+                    "launch_us": percentiles_us(pf_ms),
                     "overlapped_with_attention": True,
                     "isolated": {"value": round(iso_gbs, 2), "unit": "GB/s",
                                  "frac_link": round(iso_gbs / PEAK_PCIE5_X16_GBS, 4),
-                                 "avg_launch_us": round(iso * 1e3, 2)}}
+                                 "avg_launch_us": round(iso * 1e3, 2)},
+                    "attention_alone": {
+                        "avg_launch_us": round(sum(alone_ms) / len(alone_ms) * 1e3, 2),
+                        "launch_us": percentiles_us(alone_ms),
+                        "slowdown_beside_prefetch": round(
+                            (attn_ms / n_attn) / (sum(alone_ms) / len(alone_ms)), 4),
+                        "serial_sum_ms_per_step": round(alone_step_ms + iso * n_launch, 4),
+                        "overlapped_ms_per_step": round(ms_per_step, 4)}}
     khash = source_hash(KERNEL_SOURCES[:1])
     if pipe is not None:
         kernel_names = sorted({attention_kernel_name(b.hi - b.lo, b.max_q_len, wl.num_q_heads,
@@ -508,6 +612,8 @@ def main():
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "kernel": kernel_name,
                      "avg_launch_us": round(attn_avg_ms * 1e3, 2),
+                     "launch_us": percentiles_us(
+                         [e0.elapsed_time(e1) for row in a_ev for e0, e1 in row]),
                      "flop_per_launch": step_flops // n_launch,
                      "timing": "HIP events around every launch, in a second pass of the "
                                "same steps after the timed region"},

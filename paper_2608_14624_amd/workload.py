@@ -374,11 +374,20 @@ def _anchor_share(anchor_lens, invs):
 # --------------------------------------------------------------------------
 
 CONFIG_NAMES = ("tiny", "llama8b", "agent_batch", "llama70b_prefetch", "long_mixed",
-                "decode_batch")
+                "decode_batch", "llama70b_prefetch_tp8", "agent_batch_tp8")
+
+# one GPU's shard of a configuration split 8 ways by KV head (tensor
+# parallelism): the same invocations with Hq / 8 query and Hkv / 8 KV heads
+_TP8_OF = {"llama70b_prefetch_tp8": "llama70b_prefetch", "agent_batch_tp8": "agent_batch"}
 
 
 def config_spec(name):
     """Agents, invocations and shapes of a named configuration (no arrays)."""
+    if name in _TP8_OF:
+        spec = config_spec(_TP8_OF[name])
+        spec["num_q_heads"] //= 8
+        spec["num_kv_heads"] //= 8
+        return spec
     if name == "tiny":
         # 1 request: 256-token cached prefix + 64-token suffix, 8/2 heads, D=64,
         # pool of 64 blocks, scale 1/sqrt(64)

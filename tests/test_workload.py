@@ -103,3 +103,12 @@ def test_offpool_blocks_are_nan_until_prefetched():
     assert np.all(wl.k_pool[wl.prefetch_dst] == W.BF16_NAN)
     assert len(np.unique(wl.prefetch_dst)) == 4
     assert set(wl.prefetch_agent.tolist()) == {0, 1}
+
+
+@pytest.mark.parametrize("shard,full", [("llama70b_prefetch_tp8", "llama70b_prefetch"),
+                                        ("agent_batch_tp8", "agent_batch")])
+def test_tp8_shard_configs_are_the_full_invocations_with_an_eighth_of_the_heads(shard, full):
+    a, b = W.config_spec(shard), W.config_spec(full)
+    assert a["num_q_heads"] * 8 == b["num_q_heads"] and a["num_kv_heads"] * 8 == b["num_kv_heads"]
+    assert a["num_kv_heads"] == 1
+    assert a["invocations"] == b["invocations"] and a["anchor_lens"] == b["anchor_lens"]
