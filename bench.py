@@ -50,6 +50,9 @@ DESCRIPTIONS = {
     "decode_batch": "128 sequences over 8 agents, anchors U[4096,8192] + lognormal history "
                     "(median 512) in [128,4096], one token decoded per sequence, 32 query / 8 "
                     "KV heads, head_dim 128",
+    "decode_private": "128 sequences with the decode_batch length mix and nothing shared (each "
+                      "its own anchor U[4096,8192] + history), one token decoded per sequence, "
+                      "32 query / 8 KV heads, head_dim 128",
     "llama70b_prefetch_tp8": "one GPU's shard of llama70b_prefetch split 8 ways by KV head: "
                              "the same 16 invocations and prefetches with 8 query / 1 KV head",
     "agent_batch_tp8": "one GPU's shard of agent_batch split 8 ways by KV head: the same 32 "

@@ -374,7 +374,7 @@ def _anchor_share(anchor_lens, invs):
 # --------------------------------------------------------------------------
 
 CONFIG_NAMES = ("tiny", "llama8b", "agent_batch", "llama70b_prefetch", "long_mixed",
-                "decode_batch", "llama70b_prefetch_tp8", "agent_batch_tp8")
+                "decode_batch", "decode_private", "llama70b_prefetch_tp8", "agent_batch_tp8")
 
 # one GPU's shard of a configuration split 8 ways by KV head (tensor
 # parallelism): the same invocations with Hq / 8 query and Hkv / 8 KV heads
@@ -440,6 +440,16 @@ def config_spec(name):
         hist = np.clip(np.rint(rng.lognormal(np.log(512.0), 1.0, size=128)), 128, 4096)
         invs = [Invocation(int(a), int(s)) for a, s in zip(agents, hist)]
         return dict(seed=5, anchor_lens=anchors, invocations=invs,
+                    num_q_heads=32, num_kv_heads=8, head_dim=128, occupancy=0.9)
+    if name == "decode_private":
+        # the same length mix with nothing shared: 128 sequences, each its own
+        # agent with an anchor U[4096, 8192] + history as in decode_batch, so
+        # every key of every sequence is a distinct pool block
+        rng = np.random.default_rng([6, _K_SPEC])
+        anchors = [int(x) for x in rng.integers(4096, 8192, size=128, endpoint=True)]
+        hist = np.clip(np.rint(rng.lognormal(np.log(512.0), 1.0, size=128)), 128, 4096)
+        invs = [Invocation(a, int(s)) for a, s in enumerate(hist)]
+        return dict(seed=6, anchor_lens=anchors, invocations=invs,
                     num_q_heads=32, num_kv_heads=8, head_dim=128, occupancy=0.9)
     raise KeyError(name)
 

@@ -270,3 +270,16 @@ def test_decode_and_cascade_ignore_nan_and_inf_past_the_end():
     got = run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"],
                       cv["max_group_seqs"], cv["max_shared_len"])
     check(got, oracle_decode(q, seq_lens, bt, wl), "cascade vs oracle")
+
+
+def test_decode_private_recipe_scaled_down():
+    """The decode_private recipe (every sequence its own anchor, nothing
+    shared) at 12 sequences: per-sequence decode against the oracle."""
+    rng = np.random.default_rng([6, 1])
+    anchors = [int(x) for x in rng.integers(4096, 8192, size=12, endpoint=True)]
+    hist = np.clip(np.rint(rng.lognormal(np.log(512.0), 1.0, size=12)), 128, 4096)
+    invs = [Invocation(a, int(s)) for a, s in enumerate(hist)]
+    wl = build_workload("decode_private_small", 6, anchors, invs, num_q_heads=32, num_kv_heads=8,
+                        head_dim=128, occupancy=0.9)
+    print(f"[case] decode_private scaled down: kv_lens={wl.kv_lens.tolist()}", flush=True)
+    check(run_decode(wl), oracle_last_rows(wl), "decode vs oracle")
