@@ -210,6 +210,48 @@ def cs_prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_len
     _check(status)
 
 
+class PrefillCall:
+    """A cs_prefill_paged_attn call with its tensors validated once.
+
+    Serving loops launch the same attention over the same buffers again and
+    again; this keeps the argument checks and pointer extraction out of the
+    per-launch path, so each launch costs one C call.  The tensors must stay
+    alive and unchanged in shape while the object is used.
+    """
+
+    def __init__(self, q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out, *,
+                 max_q_len, max_kv_len, scale):
+        # the same checks as cs_prefill_paged_attn, done once
+        dev = q.device
+        for name, t, dt in (("q", q, torch.bfloat16), ("k_pool", k_pool, torch.bfloat16),
+                            ("v_pool", v_pool, torch.bfloat16), ("out", out, torch.bfloat16),
+                            ("block_tables", block_tables, torch.int32),
+                            ("prefix_lens", prefix_lens, torch.int32),
+                            ("cu_q_lens", cu_q_lens, torch.int32)):
+            _require(t.device == dev and t.is_cuda, f"{name} must be on {dev}")
+            _require(t.dtype == dt, f"{name} must be {dt}")
+            _require(t.is_contiguous(), f"{name} must be contiguous")
+        _require(q.dim() == 3 and out.shape == q.shape, "q and out must be [total_q, Hq, D]")
+        _require(k_pool.dim() == 4 and v_pool.shape == k_pool.shape,
+                 "pools must be [num_blocks, Hkv, block_size, D]")
+        _require(block_tables.dim() == 2, "block_tables must be [B, max_blocks]")
+        total_q, hq, d = q.shape
+        num_blocks, hkv, bs, d2 = k_pool.shape
+        _require(d == d2, "head_dim of q and pools differ")
+        batch = block_tables.shape[0]
+        _require(prefix_lens.numel() == batch and cu_q_lens.numel() == batch + 1,
+                 "prefix_lens must have B entries and cu_q_lens B + 1")
+        self.device = dev
+        self._keep = (q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out)
+        self._args = (_ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_tables), _ptr(prefix_lens),
+                      _ptr(cu_q_lens), batch, total_q, int(max_q_len), int(max_kv_len),
+                      block_tables.shape[1], num_blocks, hq, hkv, d, bs, ctypes.c_float(scale),
+                      _ptr(out))
+
+    def __call__(self, stream=None):
+        _check(_lib.cs_prefill_paged_attn(*self._args, _stream_handle(stream, self.device)))
+
+
 def cs_kv_prefetch(host_k, host_v, dst_block_ids, k_pool, v_pool, *, stream=None):
     """Enqueue the host-to-pool block copy on ``stream`` (default: current stream).
 

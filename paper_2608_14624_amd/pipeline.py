@@ -64,12 +64,16 @@ class SubBatch:
         self.flops = 4 * wl.head_dim * wl.num_q_heads * int(
             np.sum(qlens * wl.prefix_lens[lo:hi] + qlens * (qlens + 1) // 2))
         self.dw = dw
+        self._call = None
+        if hi > lo:
+            self._call = ops.PrefillCall(self.q, dw.k_pool, dw.v_pool, self.block_tables,
+                                         self.prefix_lens, self.cu_q_lens, self.out,
+                                         max_q_len=self.max_q_len, max_kv_len=self.max_kv_len,
+                                         scale=wl.scale)
 
     def attention(self, stream=None):
-        ops.cs_prefill_paged_attn(self.q, self.dw.k_pool, self.dw.v_pool, self.block_tables,
-                                  self.prefix_lens, self.cu_q_lens, self.out,
-                                  max_q_len=self.max_q_len, max_kv_len=self.max_kv_len,
-                                  scale=self.dw.wl.scale, stream=stream)
+        if self._call is not None:
+            self._call(stream)
 
 
 class DeviceWorkload:
@@ -85,6 +89,10 @@ class DeviceWorkload:
         self.prefix_lens = _i32(wl.prefix_lens, self.device)
         self.cu_q_lens = _i32(wl.cu_q_lens, self.device)
         self.out = torch.empty_like(self.q)
+        self._call = ops.PrefillCall(self.q, self.k_pool, self.v_pool, self.block_tables,
+                                     self.prefix_lens, self.cu_q_lens, self.out,
+                                     max_q_len=wl.max_q_len, max_kv_len=wl.max_kv_len,
+                                     scale=wl.scale)
         self.host_k = self.host_v = self.prefetch_dst = None
         if wl.prefetch_dst is not None:
             self.host_k = _to_pinned_bf16(wl.host_k)
@@ -92,10 +100,12 @@ class DeviceWorkload:
             self.prefetch_dst = _i32(wl.prefetch_dst, self.device)
 
     def attention(self, stream=None, out=None):
+        if out is None:
+            self._call(stream)
+            return
         wl = self.wl
         ops.cs_prefill_paged_attn(self.q, self.k_pool, self.v_pool, self.block_tables,
-                                  self.prefix_lens, self.cu_q_lens,
-                                  self.out if out is None else out,
+                                  self.prefix_lens, self.cu_q_lens, out,
                                   max_q_len=wl.max_q_len, max_kv_len=wl.max_kv_len,
                                   scale=wl.scale, stream=stream)
 
