@@ -584,7 +584,8 @@ __global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_page
 // a round of ping-pong tiles) runs as twice as many half tiles on the split
 // path, which fills the last round's idle CUs.  LDS: the split path's two
 // halves; a ping-pong tile uses the first.  Launches without a tail take the
-// plain kernel (one LDS half).  The ping-pong body stays in the kernel
+// plain kernel (one LDS half), or for D = 128 the direct-to-LDS kernel
+// below.  The ping-pong body stays in the kernel
 // itself: moved into a device function, it compiled to more registers and
 // ran 3-5% slower.
 template <int D, bool kTail>
@@ -909,6 +910,323 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
   else run(std::false_type{});
 }
 
+// The ping-pong kernel for D = 128 with K and V moved by buffer loads that
+// write LDS directly (buffer_load_dwordx4 ... lds), without a round trip
+// through registers: the 32 staging registers per lane go, and the loads of
+// a step have two iterations to land in a three-deep ring of K and V
+// buffers.  Buffer loads rather than global ones: the compiler's wait
+// insertion treats a global load into LDS as a flat access and then makes
+// every LDS read wait for all loads in flight; with buffer loads it keeps
+// exact counts.  Same arithmetic in the same order as the ping-pong kernel,
+// so the results are bitwise equal.
+template <int D>
+__global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Params p) {
+  static_assert(D == 128, "direct-to-LDS staging is laid out for 256-byte rows");
+  // K and V of three steps, each in its own array so that the compiler can
+  // tell a read of one from a direct load in flight into another
+  __shared__ __attribute__((aligned(16))) uint16_t k0[16 * (4 * D + 8)], k1[16 * (4 * D + 8)], k2[16 * (4 * D + 8)];
+  __shared__ __attribute__((aligned(16))) uint16_t v0[16 * (4 * D + 8)], v1[16 * (4 * D + 8)], v2[16 * (4 * D + 8)];
+  const int wg = blockIdx.x;
+  constexpr int KS = D / 16;     // MFMA k-steps over the head dim
+  constexpr int DT = D / 32;     // 32-wide output tiles over the head dim
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int qi = lane & 31;
+  const int half = lane >> 5;
+  // group A (waves 0-3) runs MFMA-first, group B (waves 4-7) VALU-first; the
+  // two waves of a SIMD belong to different groups
+  const bool group_b = __builtin_amdgcn_readfirstlane(wave) >= 4;
+
+  // ---- work tile (same order as the four-wave kernel) -----------------
+  const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
+  const int g = wg % p.num_kv_heads;
+  const int sub = wg / p.num_kv_heads;
+  const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
+  const int rest = sub / tiles_per_kv;
+  const int r = rest / p.token_tiles;
+  const int token_tile = p.token_tiles - 1 - rest % p.token_tiles;
+  const int q0 = p.cu_q_lens[r];
+  const int S = p.cu_q_lens[r + 1] - q0;
+  const int t0 = token_tile * p.span;
+  if (t0 >= S) return;
+  const int P = p.prefix_lens[r];
+  const int L = P + S;
+  const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
+  const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
+  const bool row_valid = t < S;
+  const size_t qrow = ((size_t)(q0 + (row_valid ? t : 0)) * p.num_q_heads + h) * D;
+  const int qpos = row_valid ? P + t : L - 1;               // last visible key
+  const int kv_end = P + min(S, t0 + p.span);               // keys the tile needs
+  const int n_steps = (kv_end + kBN - 1) / kBN;
+  const int n_blk = (L + kBlock - 1) / kBlock;
+  const int32_t* bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
+  // first key position some row of this wave cannot see
+  const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
+  const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
+  const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
+
+  // ---- Q^T operand: lane holds query qi, dims ks*16 + half*8 .. +7 -----
+  bf16x8 qreg[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (row_valid) v = *reinterpret_cast<const uint4*>(p.q + qrow + ks * 16 + half * 8);
+    qreg[ks] = as_bf16x8(v);
+  }
+
+  // ---- staging: waves 0-3 move K, waves 4-7 move V, straight from global
+  // memory into LDS (global_load_lds_dwordx4: lane i of an instruction lands
+  // at the instruction's LDS address + 16 i); wave w moves pool block
+  // 4*step + (w & 3).  A load moves four rows (1 KB); the four-row groups sit
+  // kGrp elements apart (16 bytes of padding), and inside a group the 16-byte
+  // chunk s of row d holds the row's chunk s ^ 4d.  K operand reads (8 rows,
+  // one chunk) and transposing V reads (4 rows, 4 chunks) are then free of
+  // bank conflicts, and every per-lane address is one register plus a
+  // constant.
+  constexpr int kGrp = 4 * D + 8;                      // elements per four-row group
+  const int slot_u = __builtin_amdgcn_readfirstlane(wave & 3);
+  const uint16_t* my_base = (group_b ? p.v_pool : p.k_pool) + (size_t)g * tile_elems;
+  const __attribute__((address_space(4))) int32_t* bt_c =
+      (const __attribute__((address_space(4))) int32_t*)bt;
+  auto block_id = [&](int step) __attribute__((always_inline)) -> int {
+    const int lb = step * (kBN / kBlock) + slot_u;
+    return (step < n_steps && lb < n_blk) ? bt_c[lb] : -1;          // -1: past the end
+  };
+  // lane i of a load: row d = i / 16 of the group, stored chunk i % 16
+  const int dma_d = lane >> 4;
+  const int dma_off = dma_d * D + 8 * ((lane & 15) ^ (4 * dma_d));
+  // a block past the end loads pool slot 0 (any valid slot): its K logits
+  // are masked and its V rows zeroed
+  auto dma = [&](uint16_t* buf, int id) __attribute__((always_inline)) {
+    const uint16_t* blk = my_base + (size_t)(id >= 0 ? id : 0) * slot_elems;
+    // a buffer descriptor over the one (block, head) tile: the loads cannot leave it
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)blk, (short)0, (int)(tile_elems * sizeof(uint16_t)), 0x00020000);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + (4 * slot_u + u) * kGrp),
+                                               16, 2 * dma_off, 2 * u * 4 * D, 0, 0);
+  };
+  // V rows past the end of the sequence (inside its last block, or whole
+  // blocks past it) overwritten with zeros once their load has landed:
+  // their probabilities are 0, but 0 times a stale NaN or Inf is NaN
+  auto zero_tail = [&](uint16_t* buf, int key0) __attribute__((always_inline)) {
+    if (key0 + kBlock > L) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (key0 + 4 * u + dma_d >= L)
+          *reinterpret_cast<uint4*>(&buf[(4 * slot_u + u) * kGrp + dma_d * D + 8 * (lane & 15)]) =
+              make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  // K operand: row mt*32 + qi (group 8 mt + qi/4, row qi%4), chunk 2 ks + half,
+  // stored at chunk half + 2 (ks%2) + 4 ((ks/2) ^ (qi%4))
+  int koff[4];
+#pragma unroll
+  for (int k2 = 0; k2 < 4; ++k2)
+    koff[k2] = (qi >> 2) * kGrp + (qi & 3) * D + 8 * half + 32 * (k2 ^ (qi & 3));
+  // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
+  // transposing reads; lane 16e + i addresses key 4*(e/2) + i/4 and dims
+  // 16*(e%2) + 4*(i%4) .. +3, an 8-byte half of chunk 4 dt + jc with
+  // jc = 2 (e%2) + (i%4)/2, stored at chunk 4 (dt ^ d) + jc of its row d
+  const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int tr_d = tr_row & 3;
+  const int tr_base = (tr_row >> 2) * kGrp + tr_d * D + 8 * (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) + 4 * (lane & 1);
+  int voff[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) voff[dt] = tr_base + 32 * (dt ^ tr_d);
+  auto v_frag = [&](const uint16_t* vbuf, int ks2, int dt) __attribute__((always_inline)) -> bf16x8 {
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + 4 * ks2 * kGrp + voff[dt]));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + 4 * ks2 * kGrp + 2 * kGrp + voff[dt]));
+    const i16x4 lohi[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8, lohi);
+  };
+
+  auto run = [&](auto group_tag) __attribute__((always_inline)) {
+    constexpr bool kB = decltype(group_tag)::value;
+    f32x16 oacc[DT];
+  #pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+    f32x16 s_acc[2];             // logits of the step whose softmax is pending
+    bf16x8 pb[kBN / 16];         // probabilities of the step whose PV is pending
+    float m_run = -INFINITY;     // running max of the raw (unscaled) logits
+    float l_part[4] = {0.f, 0.f, 0.f, 0.f};
+    const float c = p.scale_log2;
+
+    // M phase of iteration j: O += P_{j-1} V_{j-1}, then S_j = K_j Q^T
+    auto mfma_phase = [&](int j, const uint16_t* kbuf_cur, const uint16_t* vbuf_prev) __attribute__((always_inline)) {
+      __builtin_amdgcn_s_setprio(1);
+      if (j >= 1) {
+        const uint16_t* vbuf = vbuf_prev;
+  #pragma unroll
+        for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
+  #pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), pb[ks2], oacc[dt], 0, 0, 0);
+        }
+        // interleave, the reads one 16-key slice ahead of their MFMAs
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
+#pragma unroll
+        for (int ks2 = 1; ks2 < kBN / 16; ++ks2) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (j < n_steps) {
+        const uint16_t* kbuf = kbuf_cur;
+        s_acc[0] = f32x16{};
+        s_acc[1] = f32x16{};
+  #pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+  #pragma unroll
+          for (int mt = 0; mt < 2; ++mt) {
+            const uint4 a = *reinterpret_cast<const uint4*>(&kbuf[mt * 8 * kGrp + 16 * (ks & 1) + koff[ks >> 1]]);
+            s_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], s_acc[mt], 0, 0, 0);
+          }
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
+#pragma unroll
+        for (int ks = 2; ks < KS; ++ks) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
+      }
+      __builtin_amdgcn_s_setprio(0);
+    };
+
+    // V phase for step x: mask, online softmax, P_x in bf16, row sums
+    auto valu_phase = [&](int x) __attribute__((always_inline)) {
+      if (x < 0 || x >= n_steps) return;
+      const int kstart = x * kBN;
+      // accumulator register rr of tile mt holds key
+      //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
+      if (kstart + kBN - 1 > wave_qmin) {
+  #pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+  #pragma unroll
+          for (int rr = 0; rr < 16; ++rr) {
+            const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
+            s_acc[mt][rr] = (kj <= qpos) ? s_acc[mt][rr] : -INFINITY;
+          }
+        }
+      }
+      float mloc = -INFINITY;
+  #pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+  #pragma unroll
+        for (int rr = 0; rr < 16; ++rr) mloc = fmaxf(mloc, s_acc[mt][rr]);
+      }
+      mloc = pair_max(mloc);
+      // lazy rescale: move the reference max only when a row's max grew by
+      // more than 2^8 in probability (true for every row at the first step)
+      const bool grow = (mloc - m_run) * c > 8.f;
+      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+        const float m_new = grow ? mloc : m_run;
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+        m_run = m_new;
+  #pragma unroll
+        for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
+  #pragma unroll
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+      }
+      const float mc = m_run * c;
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  #pragma unroll
+      for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
+        const int mt = ks2 >> 1;
+        const int rb = (ks2 & 1) * 8;
+  #pragma unroll
+        for (int s2 = 0; s2 < 8; ++s2)
+          pb[ks2][s2] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s_acc[mt][rb + s2], c, -mc));
+        // row sum over the same bf16 probabilities the PV product uses
+        l_part[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 0, 1), ones, l_part[0], false);
+        l_part[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 2, 3), ones, l_part[1], false);
+        l_part[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 4, 5), ones, l_part[2], false);
+        l_part[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 6, 7), ones, l_part[3], false);
+      }
+    };
+
+    // ---- prologue ------------------------------------------------------
+    // K waves load K_0 and K_1, V waves V_0.  Iteration j reads K_j and
+    // V_{j-1} and issues K_{j+2} (K waves) or V_{j+1} (V waves) into the
+    // buffer of the step three back, read in iteration j-1; every wave issues
+    // exactly four loads per iteration (a step past the last loads slot 0 into
+    // a buffer nothing reads again), so waiting until at most four are in
+    // flight before the barrier completes the loads of the data read next.
+    int id_next;     // block of the step the next iteration loads, read ahead
+    if (!kB) {
+      dma(k0, block_id(0));
+      dma(k1, block_id(1));
+      id_next = block_id(2);
+    } else {
+      dma(v0, block_id(0));
+      id_next = block_id(1);
+    }
+
+    auto iteration = [&](const int j, uint16_t* kcur, uint16_t* knext2, uint16_t* vprev,
+                         uint16_t* vnext) __attribute__((always_inline)) {
+      // loads issued two iterations back have landed (vmcnt <= 4); the V
+      // block read in this iteration gets its tail zeroed; then the barrier
+      __builtin_amdgcn_s_waitcnt(0x0F74);                  // vmcnt(4)
+      if (kB && j >= 1) zero_tail(vprev, (j - 1) * kBN + slot_u * kBlock);
+      __builtin_amdgcn_s_waitcnt(0xC07F);                  // lgkmcnt(0)
+      asm volatile("s_barrier" ::: "memory");
+      const int id = id_next;
+      __builtin_amdgcn_sched_barrier(0);
+      if (!kB) dma(knext2, id);                            // K_{j+2}
+      else dma(vnext, id);                                 // V_{j+1}
+      __builtin_amdgcn_sched_barrier(0);
+      if (!kB) {
+        mfma_phase(j, kcur, vprev);
+        __builtin_amdgcn_sched_barrier(0);
+        valu_phase(j);
+      } else {
+        valu_phase(j - 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_phase(j, kcur, vprev);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      id_next = block_id(kB ? j + 2 : j + 3);
+    };
+    // buffers of iteration j: K_j in kb[j%3], K_{j+2} into kb[(j+2)%3],
+    // V_{j-1} in vb[(j+2)%3], V_{j+1} into vb[(j+1)%3]; unrolled by three so
+    // that every buffer is a constant
+    int j = 0;
+    for (; j + 2 <= n_steps; j += 3) {
+      iteration(j, k0, k2, v2, v1);
+      iteration(j + 1, k1, k0, v0, v2);
+      iteration(j + 2, k2, k1, v1, v0);
+    }
+    if (j <= n_steps) iteration(j, k0, k2, v2, v1);
+    if (j + 1 <= n_steps) iteration(j + 1, k1, k0, v0, v2);
+    const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
+    const float l_tot = pair_sum(l_run);
+    const float inv = 1.f / l_tot;
+    if (row_valid) {
+      uint16_t* orow = p.out + qrow;
+  #pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+  #pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          bf16x4 o;
+  #pragma unroll
+          for (int u = 0; u < 4; ++u) o[u] = (__bf16)(oacc[dt][rg * 4 + u] * inv);
+          *reinterpret_cast<uint2*>(orow + dt * 32 + 8 * rg + 4 * half) = __builtin_bit_cast(uint2, o);
+        }
+      }
+    }
+
+  };
+  if (group_b) run(std::true_type{});
+  else run(std::false_type{});
+}
+
 }  // namespace
 
 AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads) {
@@ -971,7 +1289,7 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
       if (tail) {
         hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<128, true>), grid, dim3(kPPThreads), 0, stream, p);
       } else {
-        hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<128, false>), grid, dim3(kPPThreads), 0, stream, p);
+        hipLaunchKernelGGL((prefill_paged_attn_ppd_kernel<128>), grid, dim3(kPPThreads), 0, stream, p);
       }
     } else if (tail) {
       hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<64, true>), grid, dim3(kPPThreads), 0, stream, p);
