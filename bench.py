@@ -89,8 +89,8 @@ def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim)
     from paper_2608_14624_amd import ops
     kernel, _, tail = ops.prefill_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads)
     if kernel == ops.ATTN_PING_PONG:
-        if head_dim == 128 and not tail:
-            return "prefill_paged_attn_ppd_kernel<128>"
+        if head_dim == 128:
+            return f"prefill_paged_attn_ppd_kernel<128, {'true' if tail else 'false'}>"
         return f"prefill_paged_attn_pp_kernel<{head_dim}, {'true' if tail else 'false'}>"
     return f"prefill_paged_attn_kernel<{head_dim}, false, true>"
 

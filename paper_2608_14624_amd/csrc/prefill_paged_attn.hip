@@ -584,8 +584,8 @@ __global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_page
 // a round of ping-pong tiles) runs as twice as many half tiles on the split
 // path, which fills the last round's idle CUs.  LDS: the split path's two
 // halves; a ping-pong tile uses the first.  Launches without a tail take the
-// plain kernel (one LDS half), or for D = 128 the direct-to-LDS kernel
-// below.  The ping-pong body stays in the kernel
+// plain kernel (one LDS half).  D = 128 runs the direct-to-LDS kernel below
+// instead.  The ping-pong body stays in the kernel
 // itself: moved into a device function, it compiled to more registers and
 // ran 3-5% slower.
 template <int D, bool kTail>
@@ -910,6 +910,276 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
   else run(std::false_type{});
 }
 
+// Tail work-group of the direct-to-LDS kernel: one half (span / 2 rows) of a
+// ping-pong tile.  Waves 0-3 take the first half of the tile's 64-key steps,
+// waves 4-7 the second; each wave loads one block of K and one of V per step
+// straight into a two-deep ring of its half (k0/k1, v0/v1 or k2/k3, v2/v3),
+// one iteration ahead (an iteration takes about 2 us, ample for a load), and
+// the halves merge through LDS at the end.  The arithmetic is that of the
+// split path of the four-wave kernel, in the same order.
+template <int D>
+__device__ __forceinline__ void ppd_tail_tile(const Params& p, const int wg, uint16_t* k0, uint16_t* k1,
+                                              uint16_t* k2, uint16_t* k3, uint16_t* v0, uint16_t* v1,
+                                              uint16_t* v2, uint16_t* v3) {
+  constexpr int KS = D / 16;     // MFMA k-steps over the head dim
+  constexpr int DT = D / 32;     // 32-wide output tiles over the head dim
+  constexpr int kGrp = 4 * D + 8;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = (tid >> 6) & 3;                 // row owner within the half
+  const int split_half = __builtin_amdgcn_readfirstlane(tid >> 8);
+  const int qi = lane & 31;
+  const int half = lane >> 5;
+
+  // ---- work tile: the halves of a ping-pong tile are num_kv_heads
+  // work-groups apart, so both run on the XCD that holds their KV head
+  const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
+  const long long jt = wg - p.pp_grid;
+  const int kvh = (int)(jt % p.num_kv_heads);
+  const long long rj = jt / p.num_kv_heads;
+  const int sub_half = (int)(rj & 1);
+  const int tile = (int)(p.pp_grid + (rj >> 1) * p.num_kv_heads + kvh);
+  const int span = p.span / 2;
+  const int g = tile % p.num_kv_heads;
+  const int sub = tile / p.num_kv_heads;
+  const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
+  const int rest = sub / tiles_per_kv;
+  const int r = rest / p.token_tiles;
+  const int token_tile = p.token_tiles - 1 - rest % p.token_tiles;
+  const int q0 = p.cu_q_lens[r];
+  const int S = p.cu_q_lens[r + 1] - q0;
+  const int t0 = token_tile * p.span + sub_half * span;
+  if (t0 >= S) return;
+  const int P = p.prefix_lens[r];
+  const int L = P + S;
+  const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
+  const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
+  const bool row_valid = t < S;
+  const size_t qrow = ((size_t)(q0 + (row_valid ? t : 0)) * p.num_q_heads + h) * D;
+  const int qpos = row_valid ? P + t : L - 1;               // last visible key
+  const int kv_end = P + min(S, t0 + span);                 // keys the tile needs
+  const int n_all = (kv_end + kBN - 1) / kBN;
+  const int n_iter = n_all - n_all / 2;                     // both halves run as many iterations
+  const int j0 = split_half ? n_all / 2 : 0;
+  const int n_steps = split_half ? n_all - n_all / 2 : n_all / 2;
+  const int n_blk = (L + kBlock - 1) / kBlock;
+  const int32_t* bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
+  const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
+  const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
+  const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
+
+  // ---- Q^T operand: lane holds query qi, dims ks*16 + half*8 .. +7 -----
+  bf16x8 qreg[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (row_valid) v = *reinterpret_cast<const uint4*>(p.q + qrow + ks * 16 + half * 8);
+    qreg[ks] = as_bf16x8(v);
+  }
+
+  // ---- staging: wave w loads pool block 4*step + w of its half's steps,
+  // K and V, in the layout of the ping-pong kernel above
+  const int slot_u = __builtin_amdgcn_readfirstlane(wave);
+  const uint16_t* kbase = p.k_pool + (size_t)g * tile_elems;
+  const uint16_t* vbase = p.v_pool + (size_t)g * tile_elems;
+  const __attribute__((address_space(4))) int32_t* bt_c =
+      (const __attribute__((address_space(4))) int32_t*)bt;
+  auto block_id = [&](int step) __attribute__((always_inline)) -> int {
+    const int lb = (j0 + step) * (kBN / kBlock) + slot_u;
+    return (step < n_steps && lb < n_blk) ? bt_c[lb] : -1;          // -1: past the end
+  };
+  const int dma_d = lane >> 4;
+  const int dma_off = dma_d * D + 8 * ((lane & 15) ^ (4 * dma_d));
+  auto dma = [&](uint16_t* buf, const uint16_t* base, int id) __attribute__((always_inline)) {
+    const uint16_t* blk = base + (size_t)(id >= 0 ? id : 0) * slot_elems;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)blk, (short)0, (int)(tile_elems * sizeof(uint16_t)), 0x00020000);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + (4 * slot_u + u) * kGrp),
+                                               16, 2 * dma_off, 2 * u * 4 * D, 0, 0);
+  };
+  auto zero_tail = [&](uint16_t* buf, int key0) __attribute__((always_inline)) {
+    if (key0 + kBlock > L) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (key0 + 4 * u + dma_d >= L)
+          *reinterpret_cast<uint4*>(&buf[(4 * slot_u + u) * kGrp + dma_d * D + 8 * (lane & 15)]) =
+              make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  int koff[4];
+#pragma unroll
+  for (int k2i = 0; k2i < 4; ++k2i)
+    koff[k2i] = (qi >> 2) * kGrp + (qi & 3) * D + 8 * half + 32 * (k2i ^ (qi & 3));
+  const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
+  const int tr_d = tr_row & 3;
+  const int tr_base = (tr_row >> 2) * kGrp + tr_d * D + 8 * (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) + 4 * (lane & 1);
+  int voff[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) voff[dt] = tr_base + 32 * (dt ^ tr_d);
+  auto v_frag = [&](const uint16_t* vbuf, int ks2, int dt) __attribute__((always_inline)) -> bf16x8 {
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + 4 * ks2 * kGrp + voff[dt]));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + 4 * ks2 * kGrp + 2 * kGrp + voff[dt]));
+    const i16x4 lohi[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8, lohi);
+  };
+
+  f32x16 oacc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
+  float m_run = -INFINITY;     // running max of the raw (unscaled) logits
+  float l_part[4] = {0.f, 0.f, 0.f, 0.f};
+  const float c = p.scale_log2;
+
+  // logits, mask, online softmax and PV product of step j
+  auto step = [&](const int j, const uint16_t* kbuf, const uint16_t* vbuf) __attribute__((always_inline)) {
+    const int kstart = (j0 + j) * kBN;
+    f32x16 s_cur[2];
+    s_cur[0] = f32x16{};
+    s_cur[1] = f32x16{};
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const uint4 a = *reinterpret_cast<const uint4*>(&kbuf[mt * 8 * kGrp + 16 * (ks & 1) + koff[ks >> 1]]);
+        s_cur[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], s_cur[mt], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_s_setprio(0);
+    // accumulator register rr of tile mt holds key
+    //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
+    if (kstart + kBN - 1 > wave_qmin) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
+          s_cur[mt][rr] = (kj <= qpos) ? s_cur[mt][rr] : -INFINITY;
+        }
+      }
+    }
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) mloc = fmaxf(mloc, s_cur[mt][rr]);
+    }
+    mloc = pair_max(mloc);
+    // lazy rescale (a row whose keys so far were all masked keeps
+    // m_run = -inf: possible only in the second half)
+    const bool grow = (mloc - m_run) * c > 8.f;
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+      const float m_new = grow ? mloc : m_run;
+      const float alpha = (m_new == m_run) ? 1.f : __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      m_run = m_new;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
+    }
+    const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr)
+        s_cur[mt][rr] = __builtin_amdgcn_exp2f(__builtin_fmaf(s_cur[mt][rr], c, -mc));
+    }
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
+      const int mt = ks2 >> 1;
+      const int rb = (ks2 & 1) * 8;
+      bf16x8 b;
+#pragma unroll
+      for (int s2 = 0; s2 < 8; ++s2) b[s2] = (__bf16)s_cur[mt][rb + s2];
+      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+      l_part[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 0, 1), ones, l_part[0], false);
+      l_part[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 2, 3), ones, l_part[1], false);
+      l_part[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 4, 5), ones, l_part[2], false);
+      l_part[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(b, b, 6, 7), ones, l_part[3], false);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), b, oacc[dt], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_setprio(0);
+  };
+
+  // iteration j: this step's loads have landed (nothing newer is in flight),
+  // V past the end zeroed, barrier; then the loads of step j+1 into the
+  // other buffer, read last in iteration j-1, and step j
+  auto run = [&](uint16_t* kr0, uint16_t* kr1, uint16_t* vr0, uint16_t* vr1) __attribute__((always_inline)) {
+    int id = block_id(0);
+    if (n_steps > 0) {
+      dma(kr0, kbase, id);
+      dma(vr0, vbase, id);
+    }
+    id = block_id(1);
+    auto iteration = [&](const int j, uint16_t* kcur, uint16_t* vcur, uint16_t* knext,
+                         uint16_t* vnext) __attribute__((always_inline)) {
+      __builtin_amdgcn_s_waitcnt(0x0F70);                  // vmcnt(0)
+      if (j < n_steps) zero_tail(vcur, (j0 + j) * kBN + slot_u * kBlock);
+      __builtin_amdgcn_s_waitcnt(0xC07F);                  // lgkmcnt(0)
+      asm volatile("s_barrier" ::: "memory");
+      if (j + 1 < n_steps) {
+        dma(knext, kbase, id);
+        dma(vnext, vbase, id);
+      }
+      if (j < n_steps) step(j, kcur, vcur);
+      id = block_id(j + 2);
+    };
+    for (int j = 0; j < n_iter; j += 2) {
+      iteration(j, kr0, vr0, kr1, vr1);
+      if (j + 1 < n_iter) iteration(j + 1, kr1, vr1, kr0, vr0);
+    }
+  };
+  if (split_half) run(k2, k3, v2, v3);
+  else run(k0, k1, v0, v1);
+
+  const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
+  float l_tot = pair_sum(l_run);
+  // ---- merge: wave w of the second half hands (O, m, l) of its rows to
+  // wave w of the first through one 16640-byte buffer: value e of lane l at
+  // word 64 e + l, m and l of query qi at words 4096 + qi and 4128 + qi
+  float* x = reinterpret_cast<float*>(wave == 0 ? k0 : wave == 1 ? k1 : wave == 2 ? v0 : v1);
+  __syncthreads();
+  if (split_half == 1) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int rr = 0; rr < 16; ++rr) x[(dt * 16 + rr) * 64 + lane] = oacc[dt][rr];
+    x[64 * 64 + 32 * half + qi] = half ? l_tot : m_run;
+  }
+  __syncthreads();
+  if (split_half == 1) return;
+  const float m1 = x[64 * 64 + qi];
+  const float l1 = x[64 * 64 + 32 + qi];
+  const float mx = fmaxf(m_run, m1);
+  const float w0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run - mx) * c);
+  const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m1 - mx) * c);
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int rr = 0; rr < 16; ++rr) oacc[dt][rr] = w0 * oacc[dt][rr] + w1 * x[(dt * 16 + rr) * 64 + lane];
+  l_tot = w0 * l_tot + w1 * l1;
+  const float inv = 1.f / l_tot;
+  if (row_valid) {
+    uint16_t* orow = p.out + qrow;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        bf16x4 o;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) o[u] = (__bf16)(oacc[dt][rg * 4 + u] * inv);
+        *reinterpret_cast<uint2*>(orow + dt * 32 + 8 * rg + 4 * half) = __builtin_bit_cast(uint2, o);
+      }
+    }
+  }
+}
+
 // The ping-pong kernel for D = 128 with K and V moved by buffer loads that
 // write LDS directly (buffer_load_dwordx4 ... lds), without a round trip
 // through registers: the 32 staging registers per lane go, and the loads of
@@ -918,15 +1188,25 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
 // insertion treats a global load into LDS as a flat access and then makes
 // every LDS read wait for all loads in flight; with buffer loads it keeps
 // exact counts.  Same arithmetic in the same order as the ping-pong kernel,
-// so the results are bitwise equal.
-template <int D>
+// so the results are bitwise equal.  kTail: as in the ping-pong kernel, the
+// work-groups from pp_grid on take half tiles of the launch's last round.
+template <int D, bool kTail>
 __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Params p) {
   static_assert(D == 128, "direct-to-LDS staging is laid out for 256-byte rows");
   // K and V of three steps, each in its own array so that the compiler can
   // tell a read of one from a direct load in flight into another
-  __shared__ __attribute__((aligned(16))) uint16_t k0[16 * (4 * D + 8)], k1[16 * (4 * D + 8)], k2[16 * (4 * D + 8)];
-  __shared__ __attribute__((aligned(16))) uint16_t v0[16 * (4 * D + 8)], v1[16 * (4 * D + 8)], v2[16 * (4 * D + 8)];
+  constexpr int kBuf = 16 * (4 * D + 8);
+  __shared__ __attribute__((aligned(16))) uint16_t k0[kBuf], k1[kBuf], k2[kBuf];
+  __shared__ __attribute__((aligned(16))) uint16_t v0[kBuf], v1[kBuf], v2[kBuf];
   const int wg = blockIdx.x;
+  if constexpr (kTail) {
+    if (wg >= p.pp_grid) {
+      // the tail's two-deep rings take two more buffers
+      __shared__ __attribute__((aligned(16))) uint16_t k3[kBuf], v3[kBuf];
+      ppd_tail_tile<D>(p, wg, k0, k1, k2, k3, v0, v1, v2, v3);
+      return;
+    }
+  }
   constexpr int KS = D / 16;     // MFMA k-steps over the head dim
   constexpr int DT = D / 32;     // 32-wide output tiles over the head dim
 
@@ -1287,9 +1567,9 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
     const bool tail = geo.grid > geo.pp_grid;
     if (a.head_dim == 128) {
       if (tail) {
-        hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<128, true>), grid, dim3(kPPThreads), 0, stream, p);
+        hipLaunchKernelGGL((prefill_paged_attn_ppd_kernel<128, true>), grid, dim3(kPPThreads), 0, stream, p);
       } else {
-        hipLaunchKernelGGL((prefill_paged_attn_ppd_kernel<128>), grid, dim3(kPPThreads), 0, stream, p);
+        hipLaunchKernelGGL((prefill_paged_attn_ppd_kernel<128, false>), grid, dim3(kPPThreads), 0, stream, p);
       }
     } else if (tail) {
       hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<64, true>), grid, dim3(kPPThreads), 0, stream, p);
