@@ -910,17 +910,19 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
   else run(std::false_type{});
 }
 
-// Tail work-group of the direct-to-LDS kernel: one half (span / 2 rows) of a
-// ping-pong tile.  Waves 0-3 take the first half of the tile's 64-key steps,
-// waves 4-7 the second; each wave loads one block of K and one of V per step
-// straight into a two-deep ring of its half (k0/k1, v0/v1 or k2/k3, v2/v3),
-// one iteration ahead (an iteration takes about 2 us, ample for a load), and
-// the halves merge through LDS at the end.  The arithmetic is that of the
-// split path of the four-wave kernel, in the same order.
-template <int D>
-__device__ __forceinline__ void ppd_tail_tile(const Params& p, const int wg, uint16_t* k0, uint16_t* k1,
-                                              uint16_t* k2, uint16_t* k3, uint16_t* v0, uint16_t* v1,
-                                              uint16_t* v2, uint16_t* v3) {
+// Split tile with direct-to-LDS staging: 8 waves over one tile of span rows
+// (a launch of less than a round of ping-pong tiles), or over one half
+// (span / 2 rows) of a ping-pong tile in a launch's last round (kTailTile).
+// Waves 0-3 take the first half of the tile's 64-key steps, waves 4-7 the
+// second; each wave loads one block of K and one of V per step straight into
+// a two-deep ring of its half (k0/k1, v0/v1 or k2/k3, v2/v3), one iteration
+// ahead (an iteration takes about 2 us, ample for a load), and the halves
+// merge through LDS at the end.  The arithmetic is that of the split path of
+// the four-wave kernel, in the same order.
+template <int D, bool kTailTile>
+__device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, uint16_t* k0, uint16_t* k1,
+                                               uint16_t* k2, uint16_t* k3, uint16_t* v0, uint16_t* v1,
+                                               uint16_t* v2, uint16_t* v3) {
   constexpr int KS = D / 16;     // MFMA k-steps over the head dim
   constexpr int DT = D / 32;     // 32-wide output tiles over the head dim
   constexpr int kGrp = 4 * D + 8;
@@ -931,15 +933,21 @@ __device__ __forceinline__ void ppd_tail_tile(const Params& p, const int wg, uin
   const int qi = lane & 31;
   const int half = lane >> 5;
 
-  // ---- work tile: the halves of a ping-pong tile are num_kv_heads
-  // work-groups apart, so both run on the XCD that holds their KV head
+  // ---- work tile (the order of the four-wave kernel); the halves of a
+  // ping-pong tile are num_kv_heads work-groups apart, so both run on the
+  // XCD that holds their KV head
   const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
-  const long long jt = wg - p.pp_grid;
-  const int kvh = (int)(jt % p.num_kv_heads);
-  const long long rj = jt / p.num_kv_heads;
-  const int sub_half = (int)(rj & 1);
-  const int tile = (int)(p.pp_grid + (rj >> 1) * p.num_kv_heads + kvh);
-  const int span = p.span / 2;
+  int tile = wg;
+  int sub_half = 0;
+  int span = p.span;
+  if constexpr (kTailTile) {
+    const long long jt = wg - p.pp_grid;
+    const int kvh = (int)(jt % p.num_kv_heads);
+    const long long rj = jt / p.num_kv_heads;
+    sub_half = (int)(rj & 1);
+    tile = (int)(p.pp_grid + (rj >> 1) * p.num_kv_heads + kvh);
+    span = p.span / 2;
+  }
   const int g = tile % p.num_kv_heads;
   const int sub = tile / p.num_kv_heads;
   const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
@@ -1203,7 +1211,7 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
     if (wg >= p.pp_grid) {
       // the tail's two-deep rings take two more buffers
       __shared__ __attribute__((aligned(16))) uint16_t k3[kBuf], v3[kBuf];
-      ppd_tail_tile<D>(p, wg, k0, k1, k2, k3, v0, v1, v2, v3);
+      ppd_split_tile<D, true>(p, wg, k0, k1, k2, k3, v0, v1, v2, v3);
       return;
     }
   }
@@ -1507,6 +1515,17 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
   else run(std::false_type{});
 }
 
+// Launches of less than one round of ping-pong tiles, D = 128: split tiles
+// (128 rows x 8 waves over two halves of the keys) with direct-to-LDS staging.
+template <int D>
+__global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_split_kernel(Params p) {
+  static_assert(D == 128, "direct-to-LDS staging is laid out for 256-byte rows");
+  constexpr int kBuf = 16 * (4 * D + 8);
+  __shared__ __attribute__((aligned(16))) uint16_t k0[kBuf], k1[kBuf], k2[kBuf], k3[kBuf];
+  __shared__ __attribute__((aligned(16))) uint16_t v0[kBuf], v1[kBuf], v2[kBuf], v3[kBuf];
+  ppd_split_tile<D, false>(p, blockIdx.x, k0, k1, k2, k3, v0, v1, v2, v3);
+}
+
 }  // namespace
 
 AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads) {
@@ -1579,7 +1598,7 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
   } else if (a.head_dim == 128) {
     // fewer than one ping-pong work-group per CU: 128-row tiles, each run
     // by 8 waves over two halves of its keys
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, false, true>), grid, dim3(2 * kThreads), 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<128>), grid, dim3(kPPThreads), 0, stream, p);
   } else {
     hipLaunchKernelGGL((prefill_paged_attn_kernel<64, false, true>), grid, dim3(2 * kThreads), 0, stream, p);
   }
