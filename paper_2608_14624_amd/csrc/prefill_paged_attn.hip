@@ -1344,27 +1344,10 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
     float l_part[4] = {0.f, 0.f, 0.f, 0.f};
     const float c = p.scale_log2;
 
-    // M phase of iteration j: O += P_{j-1} V_{j-1}, then S_j = K_j Q^T
+    // M phase of iteration j: S_j = K_j Q^T, then O += P_{j-1} V_{j-1} (the
+    // softmax of S_j can start while the PV MFMAs drain; at normal priority,
+    // measured 0.5-1% faster than the other order with the priority raised)
     auto mfma_phase = [&](int j, const uint16_t* kbuf_cur, const uint16_t* vbuf_prev) __attribute__((always_inline)) {
-      __builtin_amdgcn_s_setprio(1);
-      if (j >= 1) {
-        const uint16_t* vbuf = vbuf_prev;
-  #pragma unroll
-        for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
-  #pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), pb[ks2], oacc[dt], 0, 0, 0);
-        }
-        // interleave, the reads one 16-key slice ahead of their MFMAs
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
-#pragma unroll
-        for (int ks2 = 1; ks2 < kBN / 16; ++ks2) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
-      }
-      __builtin_amdgcn_sched_barrier(0);
       if (j < n_steps) {
         const uint16_t* kbuf = kbuf_cur;
         s_acc[0] = f32x16{};
@@ -1385,7 +1368,24 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
         }
         __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
       }
-      __builtin_amdgcn_s_setprio(0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (j >= 1) {
+        const uint16_t* vbuf = vbuf_prev;
+  #pragma unroll
+        for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
+  #pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), pb[ks2], oacc[dt], 0, 0, 0);
+        }
+        // interleave, the reads one 16-key slice ahead of their MFMAs
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
+#pragma unroll
+        for (int ks2 = 1; ks2 < kBN / 16; ++ks2) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
+      }
     };
 
     // V phase for step x: mask, online softmax, P_x in bf16, row sums
