@@ -135,6 +135,28 @@ struct Lds {
   uint16_t v[2][kBN * vStride];               // V of steps j
 };
 
+// Direct-to-LDS staging (the D = 128 kernels).  buffer_load_dwordx4 with the
+// LDS flag writes lane i's 16 bytes at the instruction's LDS address + 16 i,
+// so one load moves four 256-byte rows of a (block, head) tile (1 KB).  A
+// buffer holds one 64-key step as 16 four-row groups 4 D + 8 elements apart
+// (16 bytes of padding); inside a group, the 16-byte chunk s of row d holds
+// the row's chunk s ^ 4d.  The K operand reads (ds_read_b128: 8 rows, one
+// chunk per 8 lanes) and the transposing V reads (4 rows, 4 chunks per 32
+// lanes) are then free of bank conflicts at 64 banks, and every per-lane
+// address is one register plus a constant.  Buffer loads rather than
+// global_load_lds: the compiler's wait insertion counts a global load into
+// LDS as a flat access and then makes every LDS read wait for all loads in
+// flight; with buffer loads it keeps exact counts.
+//
+// Word 3 of a raw buffer descriptor on gfx9-family parts: 32-bit data format
+// (DATA_FORMAT = 4), no swizzle, no index stride.
+constexpr int kRawBufferWord3 = 0x00020000;
+// s_waitcnt immediates (gfx9 layout: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8],
+// vmcnt[5:4] at [15:14]; a field at its maximum does not wait)
+constexpr int kWaitVmcnt0 = 0x0F70;
+constexpr int kWaitVmcnt4 = 0x0F74;
+constexpr int kWaitLgkmcnt0 = 0xC07F;
+
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // Lanes l and l ^ 32 hold the same query row (the two halves of its keys).
@@ -986,7 +1008,7 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   }
 
   // ---- staging: wave w loads pool block 4*step + w of its half's steps,
-  // K and V, in the layout of the ping-pong kernel above
+  // K and V, in the direct-to-LDS layout
   const int slot_u = __builtin_amdgcn_readfirstlane(wave);
   const uint16_t* kbase = p.k_pool + (size_t)g * tile_elems;
   const uint16_t* vbase = p.v_pool + (size_t)g * tile_elems;
@@ -1001,7 +1023,7 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   auto dma = [&](uint16_t* buf, const uint16_t* base, int id) __attribute__((always_inline)) {
     const uint16_t* blk = base + (size_t)(id >= 0 ? id : 0) * slot_elems;
     const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)blk, (short)0, (int)(tile_elems * sizeof(uint16_t)), 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc((void*)blk, (short)0, (int)(tile_elems * sizeof(uint16_t)), kRawBufferWord3);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + (4 * slot_u + u) * kGrp),
@@ -1127,9 +1149,9 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
     id = block_id(1);
     auto iteration = [&](const int j, uint16_t* kcur, uint16_t* vcur, uint16_t* knext,
                          uint16_t* vnext) __attribute__((always_inline)) {
-      __builtin_amdgcn_s_waitcnt(0x0F70);                  // vmcnt(0)
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
       if (j < n_steps) zero_tail(vcur, (j0 + j) * kBN + slot_u * kBlock);
-      __builtin_amdgcn_s_waitcnt(0xC07F);                  // lgkmcnt(0)
+      __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
       asm volatile("s_barrier" ::: "memory");
       if (j + 1 < n_steps) {
         dma(knext, kbase, id);
@@ -1188,15 +1210,11 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   }
 }
 
-// The ping-pong kernel for D = 128 with K and V moved by buffer loads that
-// write LDS directly (buffer_load_dwordx4 ... lds), without a round trip
-// through registers: the 32 staging registers per lane go, and the loads of
-// a step have two iterations to land in a three-deep ring of K and V
-// buffers.  Buffer loads rather than global ones: the compiler's wait
-// insertion treats a global load into LDS as a flat access and then makes
-// every LDS read wait for all loads in flight; with buffer loads it keeps
-// exact counts.  Same arithmetic in the same order as the ping-pong kernel,
-// so the results are bitwise equal.  kTail: as in the ping-pong kernel, the
+// The ping-pong kernel for D = 128 with direct-to-LDS staging: no round trip
+// through registers, so the 32 staging registers per lane go, and the loads
+// of a step have two iterations to land in a three-deep ring of K and V
+// buffers.  Same arithmetic in the same order as the ping-pong kernel, so
+// the results are bitwise equal.  kTail: as in the ping-pong kernel, the
 // work-groups from pp_grid on take half tiles of the launch's last round.
 template <int D, bool kTail>
 __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Params p) {
@@ -1265,14 +1283,8 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
   }
 
   // ---- staging: waves 0-3 move K, waves 4-7 move V, straight from global
-  // memory into LDS (global_load_lds_dwordx4: lane i of an instruction lands
-  // at the instruction's LDS address + 16 i); wave w moves pool block
-  // 4*step + (w & 3).  A load moves four rows (1 KB); the four-row groups sit
-  // kGrp elements apart (16 bytes of padding), and inside a group the 16-byte
-  // chunk s of row d holds the row's chunk s ^ 4d.  K operand reads (8 rows,
-  // one chunk) and transposing V reads (4 rows, 4 chunks) are then free of
-  // bank conflicts, and every per-lane address is one register plus a
-  // constant.
+  // memory into LDS in the direct-to-LDS layout; wave w moves pool block
+  // 4*step + (w & 3)
   constexpr int kGrp = 4 * D + 8;                      // elements per four-row group
   const int slot_u = __builtin_amdgcn_readfirstlane(wave & 3);
   const uint16_t* my_base = (group_b ? p.v_pool : p.k_pool) + (size_t)g * tile_elems;
@@ -1291,7 +1303,7 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
     const uint16_t* blk = my_base + (size_t)(id >= 0 ? id : 0) * slot_elems;
     // a buffer descriptor over the one (block, head) tile: the loads cannot leave it
     const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)blk, (short)0, (int)(tile_elems * sizeof(uint16_t)), 0x00020000);
+        __builtin_amdgcn_make_buffer_rsrc((void*)blk, (short)0, (int)(tile_elems * sizeof(uint16_t)), kRawBufferWord3);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + (4 * slot_u + u) * kGrp),
@@ -1461,9 +1473,9 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
                          uint16_t* vnext) __attribute__((always_inline)) {
       // loads issued two iterations back have landed (vmcnt <= 4); the V
       // block read in this iteration gets its tail zeroed; then the barrier
-      __builtin_amdgcn_s_waitcnt(0x0F74);                  // vmcnt(4)
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt4);
       if (kB && j >= 1) zero_tail(vprev, (j - 1) * kBN + slot_u * kBlock);
-      __builtin_amdgcn_s_waitcnt(0xC07F);                  // lgkmcnt(0)
+      __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
       asm volatile("s_barrier" ::: "memory");
       const int id = id_next;
       __builtin_amdgcn_sched_barrier(0);
