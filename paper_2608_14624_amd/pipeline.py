@@ -213,6 +213,10 @@ class AgentPipeline:
         self.side = side_stream if side_stream is not None else torch.cuda.Stream(dw.device)
         self.events = {a: torch.cuda.Event() for a in order}       # prefetch done
         self.attn_done = {a: torch.cuda.Event() for a in order}    # last reader done
+        # known order only: the previous pass ended / the first agent's
+        # attention of this pass is done (the only readers a prefetch can race)
+        self.pass_done = torch.cuda.Event()
+        self.first_done = torch.cuda.Event()
         self.flops = sum(b.flops for b in self.batches)
         self.prefetch_bytes = sum(int(k.numel() * 2 + v.numel() * 2)
                                   for k, v, _ in self.prefetch.values())
@@ -238,12 +242,23 @@ class AgentPipeline:
         """
         main = torch.cuda.current_stream(self.dw.device)
         n = len(self.agents)
+        known = self.policy is None
         for k, a in enumerate(self.agents):
             nxt = self.agents[(k + 1) % n]
-            target = nxt if self.policy is None else self.policy.on_turn(a)
+            target = nxt if known else self.policy.on_turn(a)
             (p0, p1), (a0, a1) = timing[k] if timing is not None else ((None, None),) * 2
             if target is not None and target != a:
-                self.side.wait_event(self.attn_done[target])
+                # wait for the last attention that read the target's slots.
+                # Known order: for turns 0 .. n-2 that was in the previous
+                # pass (one wait at turn 0 covers them); the last turn's
+                # target is the first agent, read at turn 0 of this pass.
+                # Two cross-stream events per pass instead of one per turn.
+                if not known:
+                    self.side.wait_event(self.attn_done[target])
+                elif k == 0:
+                    self.side.wait_event(self.pass_done)
+                elif k == n - 1:
+                    self.side.wait_event(self.first_done)
                 with torch.cuda.stream(self.side):
                     if p0 is not None:
                         p0.record(self.side)
@@ -260,7 +275,12 @@ class AgentPipeline:
             self.batches[k].attention(stream=main)
             if a1 is not None:
                 a1.record(main)
-            self.attn_done[a].record(main)
+            if not known:
+                self.attn_done[a].record(main)
+            elif k == 0:
+                self.first_done.record(main)
+            if known and k == n - 1:
+                self.pass_done.record(main)
             if target == nxt:
                 self.hits += 1
                 main.wait_event(self.events[nxt])
