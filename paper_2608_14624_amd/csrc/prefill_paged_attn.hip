@@ -1273,18 +1273,13 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
   const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
   const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
 
-  // ---- Q^T operand: lane holds query qi, dims ks*16 + half*8 .. +7, times
-  // scale log2(e) (rounded to bf16: a relative error of at most 2^-9 per
-  // element, below the bf16 rounding of the probabilities), so that the
-  // logits come out of the MFMA in log2 units -----
+  // ---- Q^T operand: lane holds query qi, dims ks*16 + half*8 .. +7 -----
   bf16x8 qreg[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     uint4 v = make_uint4(0, 0, 0, 0);
     if (row_valid) v = *reinterpret_cast<const uint4*>(p.q + qrow + ks * 16 + half * 8);
-    const bf16x8 raw = as_bf16x8(v);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) qreg[ks][e] = (__bf16)((float)raw[e] * p.scale_log2);
+    qreg[ks] = as_bf16x8(v);
   }
 
   // ---- staging: waves 0-3 move K, waves 4-7 move V, straight from global
@@ -1357,13 +1352,9 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
     for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
     f32x16 s_acc[2];             // logits of the step whose softmax is pending
     bf16x8 pb[kBN / 16];         // probabilities of the step whose PV is pending
+    float m_run = -INFINITY;     // running max of the raw (unscaled) logits
     float l_part[4] = {0.f, 0.f, 0.f, 0.f};
-    // reference max of the scaled logits; the QK^T accumulators start at
-    // -mc, so they hold s c - mc and a probability is one exp2
-    float mc = 0.f;
-    f32x16 bias;
-  #pragma unroll
-    for (int r = 0; r < 16; ++r) bias[r] = 0.f;
+    const float c = p.scale_log2;
 
     // M phase of iteration j: S_j = K_j Q^T, then O += P_{j-1} V_{j-1} (the
     // softmax of S_j can start while the PV MFMAs drain; at normal priority,
@@ -1371,12 +1362,14 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
     auto mfma_phase = [&](int j, const uint16_t* kbuf_cur, const uint16_t* vbuf_prev) __attribute__((always_inline)) {
       if (j < n_steps) {
         const uint16_t* kbuf = kbuf_cur;
+        s_acc[0] = f32x16{};
+        s_acc[1] = f32x16{};
   #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
   #pragma unroll
           for (int mt = 0; mt < 2; ++mt) {
             const uint4 a = *reinterpret_cast<const uint4*>(&kbuf[mt * 8 * kGrp + 16 * (ks & 1) + koff[ks >> 1]]);
-            s_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], ks == 0 ? bias : s_acc[mt], 0, 0, 0);
+            s_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], s_acc[mt], 0, 0, 0);
           }
         }
         __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
@@ -1396,7 +1389,8 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
           for (int dt = 0; dt < DT; ++dt)
             oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), pb[ks2], oacc[dt], 0, 0, 0);
         }
-        // interleave, the reads two fragments ahead of their MFMAs
+        // interleave, the reads two fragments ahead of their MFMAs (12 VGPRs
+        // of V fragments live instead of a whole 16-key slice's 32)
         __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
         for (int f = 2; f < DT * (kBN / 16); ++f) {
@@ -1431,24 +1425,18 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
       }
       mloc = pair_max(mloc);
       // lazy rescale: move the reference max only when a row's max grew by
-      // more than 2^8 in probability; at the first step every row takes its
-      // max (O and l are still zero then)
-      const bool grow = x == 0 || mloc > 8.f;
+      // more than 2^8 in probability (true for every row at the first step)
+      const bool grow = (mloc - m_run) * c > 8.f;
       if (__builtin_amdgcn_ballot_w64(grow) != 0) {
-        const float d = grow ? mloc : 0.f;
-        if (x > 0) {
-          const float alpha = __builtin_amdgcn_exp2f(-d);
+        const float m_new = grow ? mloc : m_run;
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+        m_run = m_new;
   #pragma unroll
-          for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
+        for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
   #pragma unroll
-          for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-        }
-        mc += d;
-  #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) s_acc[mt] -= d;
-  #pragma unroll
-        for (int r = 0; r < 16; ++r) bias[r] = -mc;
+        for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
       }
+      const float mc = m_run * c;
       const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   #pragma unroll
       for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
@@ -1456,7 +1444,7 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
         const int rb = (ks2 & 1) * 8;
   #pragma unroll
         for (int s2 = 0; s2 < 8; ++s2)
-          pb[ks2][s2] = (__bf16)__builtin_amdgcn_exp2f(s_acc[mt][rb + s2]);
+          pb[ks2][s2] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s_acc[mt][rb + s2], c, -mc));
         // row sum over the same bf16 probabilities the PV product uses
         l_part[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 0, 1), ones, l_part[0], false);
         l_part[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 2, 3), ones, l_part[1], false);

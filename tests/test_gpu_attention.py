@@ -118,6 +118,21 @@ def test_ping_pong_launch_with_split_tail(P, name):
     check_full(P, wl)
 
 
+@pytest.mark.parametrize("shape", ["ping_pong", "ping_pong_tail"])
+def test_peaky_logits_on_the_ping_pong_paths(P, shape):
+    """Queries scaled up 8x (logits in the tens of log2 units): the large
+    launches' kernels keep the scale in fp32 and stay within tolerance too."""
+    ops, _ = P
+    invs = {"ping_pong": [Invocation(i % 2, 1000 + 13 * i) for i in range(2)],
+            "ping_pong_tail": [Invocation(i % 2, 450 + 7 * i) for i in range(5)]}[shape]
+    wl = build_workload("peaky_pp", 8, [61, 200], invs, num_q_heads=32, num_kv_heads=8,
+                        head_dim=128, num_blocks=512, q_gain=8.0)
+    kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, 32, 8)
+    assert kernel == ops.ATTN_PING_PONG and (tail > 0) == (shape == "ping_pong_tail")
+    print(f"[case] peaky logits, {shape}: grid={grid} tail={tail}", flush=True)
+    check_full(P, wl)
+
+
 @pytest.mark.parametrize("shape", ["split", "ping_pong", "ping_pong_tail"])
 def test_nan_and_inf_past_the_end_do_not_leak(P, shape):
     """Pool positions past a sequence's end inside its last block may hold
