@@ -1078,6 +1078,14 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
         s_cur[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], s_cur[mt], 0, 0, 0);
       }
     }
+    // interleave, the K reads two k-steps ahead of their MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 2);
+#pragma unroll
+    for (int ks = 2; ks < KS; ++ks) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 2);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 2);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 2);
     __builtin_amdgcn_s_setprio(0);
     // accumulator register rr of tile mt holds key
     //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
@@ -1134,6 +1142,14 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
       for (int dt = 0; dt < DT; ++dt)
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), b, oacc[dt], 0, 0, 0);
     }
+    // interleave, the V reads two fragments ahead of their MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 3);
+#pragma unroll
+    for (int f = 2; f < DT * (kBN / 16); ++f) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 3);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 3);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 3);
     __builtin_amdgcn_s_setprio(0);
   };
 
