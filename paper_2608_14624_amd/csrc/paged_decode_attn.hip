@@ -10,12 +10,13 @@
 // not by the matrix cores.
 //
 // Kernel design
-//   * One work-group = 4 wave64s = one (sequence, KV head); the G query heads
-//     of the group are the N = 16 columns of v_mfma_f32_16x16x32_bf16 (G <= 16).
-//   * The 4 waves split the key range in 32-key chunks (wave w takes chunks
-//     w, w+4, ...) and run independent online softmaxes, so there is no
-//     synchronisation in the loop; the four partial results are merged in
-//     LDS at the end (log-sum-exp weights), so no workspace is needed.
+//   * One work-group = W wave64s = one (sequence, KV head), W = 12 (4 in
+//     cascade mode); the G query heads of the group are the N = 16 columns
+//     of v_mfma_f32_16x16x32_bf16 (G <= 16).
+//   * The W waves split the key range in 32-key chunks (wave w takes chunks
+//     w, w+W, ...) and run independent online softmaxes, so there is no
+//     synchronisation in the loop; the W partial results are merged in LDS
+//     at the end (log-sum-exp weights), so no workspace is needed.
 //   * S^T = K Q^T with K fragments loaded from HBM straight into the MFMA A
 //     operand (16 B per lane), Q^T kept in VGPRs.  O^T = V^T P^T reads V^T
 //     with ds_read_b64_tr_b16 from a per-wave LDS tile that the wave itself
@@ -47,8 +48,13 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int kBlock = 16;
 constexpr int kChunk = 32;           // keys per wave step (2 pool blocks)
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
+// waves per work-group: 12 for plain decode (one work-group fills a CU at
+// three waves per SIMD, so a CU's last, longest sequence runs on all of its
+// wave slots instead of a third of them), 4 for the cascade's 1024-key
+// segments
+constexpr int kDecodeWaves = 12;
+constexpr int kCascadeWaves = 4;
+constexpr int kThreads = 256;        // the merge kernel
 constexpr int kMaxGroup = 16;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -87,17 +93,17 @@ __device__ __forceinline__ int shared_len_of(const DecParams& p, int r) {
   return p.shared_lens[lo];
 }
 
-template <int D>
+template <int D, int W>
 struct DecLds {
   // V tile of one wave: 32 keys x D, rows padded by 32 B so that the 32 lanes
   // of a transposing read (8 keys x 32 B) fall on distinct banks.
   static constexpr int vStride = D + 16;
   union {
-    uint16_t v[kWaves][kChunk * vStride];
+    uint16_t v[W][kChunk * vStride];
     struct {
-      float m[kWaves][kMaxGroup];
-      float l[kWaves][kMaxGroup];
-      float o[kWaves][kMaxGroup][D];
+      float m[W][kMaxGroup];
+      float l[W][kMaxGroup];
+      float o[W][kMaxGroup][D];
     } merge;
   };
 };
@@ -105,9 +111,11 @@ struct DecLds {
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 template <int D, bool kCascade>
-__global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p) {
-  __shared__ DecLds<D> sm;
-  constexpr int vStride = DecLds<D>::vStride;
+__global__ __launch_bounds__(64 * (kCascade ? kCascadeWaves : kDecodeWaves)) void paged_decode_attn_kernel(DecParams p) {
+  constexpr int kWaves = kCascade ? kCascadeWaves : kDecodeWaves;
+  constexpr int kWGThreads = 64 * kWaves;
+  __shared__ DecLds<D, kWaves> sm;
+  constexpr int vStride = DecLds<D, kWaves>::vStride;
   constexpr int DC = D / 32;         // 32-wide k-steps of the QK^T product
   constexpr int DT = D / 16;         // 16-row output tiles over the head dim
   constexpr int kRowChunks = D / 8;  // 16-byte chunks per key row
@@ -272,7 +280,7 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
       oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(v_frag(dt), pb, oacc[dt], 0, 0, 0);
   }
 
-  // ---- merge the four waves' partial softmaxes ------------------------
+  // ---- merge the waves' partial softmaxes -----------------------------
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
   __syncthreads();                     // every wave is done with its V tile
@@ -286,7 +294,7 @@ __global__ __launch_bounds__(kThreads) void paged_decode_attn_kernel(DecParams p
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr) sm.merge.o[wave][j][16 * dt + 4 * qd + rr] = oacc[dt][rr];
   __syncthreads();
-  for (int idx = threadIdx.x; idx < p.group * D; idx += kThreads) {
+  for (int idx = threadIdx.x; idx < p.group * D; idx += kWGThreads) {
     const int hj = idx / D;
     const int d = idx % D;
     const size_t row = (size_t)r * p.num_q_heads + g * p.group + hj;
@@ -389,7 +397,7 @@ hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream) {
   p.num_kv_heads = a.num_kv_heads;
   p.group = a.num_q_heads / a.num_kv_heads;
   p.scale_log2 = a.scale * kLog2e;
-  const dim3 grid((unsigned)((long long)a.batch * a.num_kv_heads)), block(kThreads);
+  const dim3 grid((unsigned)((long long)a.batch * a.num_kv_heads)), block(64 * kDecodeWaves);
   if (a.head_dim == 128) {
     hipLaunchKernelGGL((paged_decode_attn_kernel<128, false>), grid, block, 0, stream, p);
   } else {
@@ -425,7 +433,7 @@ hipError_t launch_cascade_decode_rest(const CascadeLaunch& a, hipStream_t stream
   p.ws_rows = a.batch * a.num_q_heads;
   const long long rows = (long long)a.batch * a.num_kv_heads;
   if (geo.segments > 0) {
-    const dim3 grid((unsigned)(rows * geo.segments)), block(kThreads);
+    const dim3 grid((unsigned)(rows * geo.segments)), block(64 * kCascadeWaves);
     if (a.head_dim == 128) {
       hipLaunchKernelGGL((paged_decode_attn_kernel<128, true>), grid, block, 0, stream, p);
     } else {
