@@ -350,7 +350,7 @@ __global__ __launch_bounds__(kThreads) void cascade_merge_kernel(DecParams p) {
     l_s[hj * stride + i] = ml.y;
   }
   __syncthreads();
-  if (threadIdx.x < p.group) {
+  if ((int)threadIdx.x < p.group) {
     const int hj = threadIdx.x;
     float mx = -INFINITY;
     for (int i = 0; i < n; ++i) mx = fmaxf(mx, m_s[hj * stride + i]);
