@@ -79,3 +79,22 @@ def poison_tails(wl, bits=(BF16_QNAN, BF16_POS_INF)):
             wl.v_pool[slot, :, pos, :] = v
             n += 1
     return n
+
+
+def poison_slot_zero(wl, bits=BF16_QNAN):
+    """Move whatever pool slot 0 holds to a slot no sequence reads, rename it
+    in the block tables, and fill slot 0 with NaN (K and V, all heads): the
+    kernels load slot 0 in place of blocks past a sequence's end, and those
+    loads must stay masked (K) or zeroed (V).  Returns the slot used."""
+    used = set(int(x) for r in range(wl.batch)
+               for x in wl.block_tables[r, :-(-int(wl.prefix_lens[r] + wl.q_lens[r]) // wl.block_size)])
+    free = [s for s in range(1, wl.num_blocks) if s not in used]
+    assert free, "the pool needs a slot no sequence reads"
+    u = free[0]
+    for pool in (wl.k_pool, wl.v_pool):
+        pool[u] = pool[0]
+        pool[0] = np.uint16(bits)
+    bt = wl.block_tables
+    bt[bt == 0] = u
+    return u
+

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import MAX_ABS, MEAN_ABS, compare_full, compare_rows, poison_tails, sample_rows
+from gpu_util import MAX_ABS, MEAN_ABS, compare_full, compare_rows, poison_slot_zero, poison_tails, sample_rows
 from paper_2608_14624_amd.workload import Invocation, build_workload, make_config
 
 pytestmark = pytest.mark.gpu
@@ -115,6 +115,21 @@ def test_ping_pong_launch_with_split_tail(P, name):
     kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, hq, hkv)
     print(f"[case] {name}: grid={grid} tail work-groups={tail}", flush=True)
     assert kernel == ops.ATTN_PING_PONG and tail > 0
+    check_full(P, wl)
+
+
+@pytest.mark.parametrize("shape", ["split", "ping_pong", "ping_pong_tail"])
+def test_slot_zero_full_of_nan(P, shape):
+    """Blocks past a sequence's end are loaded from pool slot 0 and then
+    masked (K) or zeroed (V): with slot 0 all NaN the output stays exact."""
+    ops, _ = P
+    invs = {"split": [Invocation(0, 37), Invocation(1, 90), Invocation(0, 5)],
+            "ping_pong": [Invocation(i % 2, 1000 + 13 * i) for i in range(2)],
+            "ping_pong_tail": [Invocation(i % 2, 450 + 7 * i) for i in range(5)]}[shape]
+    wl = build_workload("nan_slot0", 6, [61, 200], invs, num_q_heads=32, num_kv_heads=8,
+                        head_dim=128, num_blocks=512)
+    u = poison_slot_zero(wl)
+    print(f"[case] slot 0 all NaN, {shape}: its blocks moved to slot {u}", flush=True)
     check_full(P, wl)
 
 
