@@ -1090,13 +1090,13 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
     // accumulator register rr of tile mt holds key
     //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
     if (kstart + kBN - 1 > wave_qmin) {
+      // key kj <= qpos  <=>  its constant offset in the step <= lim
+      const int lim = qpos - kstart - 4 * half;
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
-          s_cur[mt][rr] = (kj <= qpos) ? s_cur[mt][rr] : -INFINITY;
-        }
+        for (int rr = 0; rr < 16; ++rr)
+          s_cur[mt][rr] = (mt * 32 + 8 * (rr >> 2) + (rr & 3) <= lim) ? s_cur[mt][rr] : -INFINITY;
       }
     }
     float mloc = -INFINITY;
@@ -1424,13 +1424,13 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
       // accumulator register rr of tile mt holds key
       //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
       if (kstart + kBN - 1 > wave_qmin) {
+        // key kj <= qpos  <=>  its constant offset in the step <= lim
+        const int lim = qpos - kstart - 4 * half;
   #pragma unroll
         for (int mt = 0; mt < 2; ++mt) {
   #pragma unroll
-          for (int rr = 0; rr < 16; ++rr) {
-            const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
-            s_acc[mt][rr] = (kj <= qpos) ? s_acc[mt][rr] : -INFINITY;
-          }
+          for (int rr = 0; rr < 16; ++rr)
+            s_acc[mt][rr] = (mt * 32 + 8 * (rr >> 2) + (rr & 3) <= lim) ? s_acc[mt][rr] : -INFINITY;
         }
       }
       float mloc = -INFINITY;
