@@ -225,7 +225,7 @@ int cs_paged_decode_attn(const void *q, const void *k_pool, const void *v_pool,
  * cu_groups[g] .. cu_groups[g+1]-1, whose first shared_lens[g] keys are the
  * same pool blocks (identical block-table entries).  For each group and KV
  * head the queries of all its sequences (and of the query heads of that KV
- * head) are stacked and attend once over the shared keys, in chunks of 512
+ * head) are stacked and attend once over the shared keys, in chunks of 1024
  * keys; each chunk leaves a partial result (O relative to its running max m,
  * m and the sum l) in the workspace.  Each sequence's own keys
  * shared_lens[g] .. seq_lens[r]-1 are attended in segments of 1024 keys,
@@ -247,7 +247,7 @@ int cs_paged_decode_attn(const void *q, const void *k_pool, const void *v_pool,
  *                   and the workspace.
  *   max_rest_len    host bound on every sequence's own keys,
  *                   seq_lens[r] - shared_lens[g] <= max_rest_len <= max_seq_len.
- *                   ceil(max_shared_len / 512) + ceil(max_rest_len / 1024)
+ *                   ceil(max_shared_len / 1024) + ceil(max_rest_len / 1024)
  *                   above 512 is CS_ERR_UNSUPPORTED.
  *   workspace       device, 16-byte aligned, caller-owned scratch of at least
  *                   cs_cascade_decode_workspace_bytes(batch, num_q_heads,
@@ -267,7 +267,7 @@ int cs_cascade_decode_attn(const void *q, const void *k_pool, const void *v_pool
                            int64_t workspace_bytes, void *out, cs_stream_t stream);
 
 /* Workspace bytes cs_cascade_decode_attn needs:
- * (ceil(max_shared_len / 512) + ceil(max_rest_len / 1024)) * batch *
+ * (ceil(max_shared_len / 1024) + ceil(max_rest_len / 1024)) * batch *
  * num_q_heads * (head_dim + 2) * 4; -1 for a negative size or a zero head
  * count or head_dim. */
 int64_t cs_cascade_decode_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t head_dim,

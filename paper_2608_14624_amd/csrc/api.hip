@@ -464,7 +464,7 @@ int cs_cascade_decode_attn(const void* q, const void* k_pool, const void* v_pool
   if (geo.grid > 0x7fffffffLL || (long long)batch * num_kv_heads * geo.segments > 0x7fffffffLL)
     return fail(CS_ERR_INVALID_ARG, "launch too large");
   if (geo.chunks + geo.segments > cs::kCascadeMaxParts)
-    return fail(CS_ERR_UNSUPPORTED, "%d partials per row (max %d): max_shared_len / 512 + "
+    return fail(CS_ERR_UNSUPPORTED, "%d partials per row (max %d): max_shared_len / 1024 + "
                 "max_rest_len / 1024 too large", geo.chunks + geo.segments, cs::kCascadeMaxParts);
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (debug_checks_enabled()) {

@@ -100,7 +100,7 @@ hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream);
 // chunks of kCascadeChunkSteps * 64 keys whose partial results go to a
 // workspace; the decode kernel attends each sequence's own keys in segments
 // of kCascadeSegmentKeys, also as partials; a merge kernel combines them.
-constexpr int kCascadeChunkSteps = 8;
+constexpr int kCascadeChunkSteps = 16;
 // keys of a sequence's own part per work-group of the rest-of-sequence launch
 constexpr int kCascadeSegmentKeys = 1024;
 // partials per row the merge stages in LDS (16 heads x 512 x 8 B = 64 KiB)

@@ -28,7 +28,7 @@
 // Cascade mode: a sequence belongs to a group whose shared prefix (its first
 // shared_len keys) is attended by the stacked prefill kernel, which leaves
 // one partial result (O relative to its running max m, the max m and the sum
-// l) per 512-key chunk in a workspace.  Here a work-group takes one KV head
+// l) per 1024-key chunk in a workspace.  Here a work-group takes one KV head
 // and one 1024-key segment of a sequence's own keys shared_len .. L - 1, so
 // a long history spreads over several work-groups, and leaves its partial
 // in the workspace too; cascade_merge_kernel then combines every partial of

@@ -191,11 +191,12 @@ CGOOD = dict(DGOOD, cu_groups=FAKE, shared_lens=FAKE, num_groups=2, max_group_se
 
 
 def test_cascade_workspace_bytes():
-    # (ceil(max_shared_len / 512) + ceil(max_rest_len / 1024)) parts x batch x Hq x (D + 2) floats
+    # (ceil(max_shared_len / 1024) + ceil(max_rest_len / 1024)) parts x batch x Hq x (D + 2) floats
     assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 0, 0) == 0
     assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 64, 0) == 1 * 4 * 8 * 130 * 4
-    assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 513, 0) == 2 * 4 * 8 * 130 * 4
-    assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 513, 1025) == 4 * 4 * 8 * 130 * 4
+    assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 1024, 0) == 1 * 4 * 8 * 130 * 4
+    assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 1025, 0) == 2 * 4 * 8 * 130 * 4
+    assert ops.cs_cascade_decode_workspace_bytes(4, 8, 128, 1025, 1025) == 4 * 4 * 8 * 130 * 4
     assert ops.cs_cascade_decode_workspace_bytes(4, 8, 64, 0, 1) == 1 * 4 * 8 * 66 * 4
     assert ops.cs_cascade_decode_workspace_bytes(-1, 8, 128, 64, 0) == -1
     assert ops.cs_cascade_decode_workspace_bytes(4, 0, 128, 64, 0) == -1
@@ -213,8 +214,8 @@ def test_cascade_workspace_bytes():
     (dict(max_shared_len=101), ops.CS_ERR_INVALID_ARG),     # beyond max_seq_len
     (dict(max_shared_len=-16), ops.CS_ERR_INVALID_ARG),
     (dict(max_rest_len=101), ops.CS_ERR_INVALID_ARG),      # beyond max_seq_len
-    (dict(max_seq_len=400000, max_blocks_per_seq=25000, max_shared_len=300000,
-          max_rest_len=100000, workspace_bytes=1 << 40), ops.CS_ERR_UNSUPPORTED),   # 684 partials
+    (dict(max_seq_len=600000, max_blocks_per_seq=37500, max_shared_len=500000,
+          max_rest_len=100000, workspace_bytes=1 << 40), ops.CS_ERR_UNSUPPORTED),   # 587 partials
     (dict(max_rest_len=-1), ops.CS_ERR_INVALID_ARG),
     (dict(cu_groups=None), ops.CS_ERR_INVALID_ARG),
     (dict(shared_lens=None), ops.CS_ERR_INVALID_ARG),
