@@ -100,6 +100,8 @@ TAIL = {
     "tail_g2_d64": ([90, 17], [Invocation(i % 2, n) for i, n in
                                enumerate([640, 600, 1, 129, 300, 0, 77])], 16, 8, 64),
     "tail_g1": ([200], [Invocation(0, 512 - 29 * i) for i in range(17)], 8, 8, 128),
+    "tail_g2_d128": ([90, 17], [Invocation(i % 2, n) for i, n in
+                                enumerate([640, 600, 1, 129, 300, 0, 77])], 16, 8, 128),
     # every tile needs one 64-key step: the first key half of a tail tile
     # has no step at all and the second holds every key
     "tail_one_step": ([16, 5], [Invocation(i % 2, 1 + (7 * i) % 48) for i in range(40)], 32, 8, 128),
