@@ -304,7 +304,8 @@ def bench_copy(args, dev):
         "cascade_decode": ("prefill_paged_attn_kernel<128, true, false> + paged_decode_attn_kernel<128, true>"
                            " + cascade_merge_kernel<128>",
                            ("paper_2608_14624_amd/csrc/prefill_paged_attn.hip",
-                            "paper_2608_14624_amd/csrc/paged_decode_attn.hip")),
+                            "paper_2608_14624_amd/csrc/paged_decode_attn.hip",
+                            "paper_2608_14624_amd/csrc/internal.h")),
         "kv_write": ("kv_write_kernel", ("paper_2608_14624_amd/csrc/kv_copy.hip",)),
         "kv_offload": ("kv_offload_kernel", ("paper_2608_14624_amd/csrc/kv_copy.hip",
                                              "paper_2608_14624_amd/csrc/block_copy.h")),
