@@ -422,6 +422,51 @@ def bench_control_plane(args):
                              "sample": f"first {n_or} touches of the same trace"}}
 
 
+# (prefix, suffix, invocations, query heads, KV heads, head_dim): one agent's
+# invocations, all hits on the same prefix
+SWEEP = [(0, 512, 16, 32, 8, 128), (2048, 512, 16, 32, 8, 128), (4096, 512, 16, 32, 8, 128),
+         (2048, 2048, 4, 32, 8, 128), (8192, 1024, 4, 32, 8, 128), (1024, 128, 64, 32, 8, 128),
+         (4096, 512, 16, 64, 8, 128), (2048, 1024, 8, 16, 8, 128), (2048, 1024, 8, 8, 8, 128),
+         (2048, 512, 16, 32, 8, 64)]
+
+
+def bench_attn_sweep(args, dev):
+    """Prefill attention alone, one launch per shape, back to back with HIP
+    events on the launch stream; value = geometric mean of the shapes' rates."""
+    import math
+    import torch
+    from paper_2608_14624_amd import ops, pipeline
+    from paper_2608_14624_amd.workload import Invocation, build_workload
+    stream = torch.cuda.current_stream(dev)
+    rows = []
+    for i, (P, S, B, hq, hkv, d) in enumerate(SWEEP):
+        nb = P // 16 + B * (-(-(P % 16 + S) // 16) + 1) + 64
+        wl = build_workload(f"sweep{i}", 40 + i, [P], [Invocation(0, S) for _ in range(B)],
+                            num_q_heads=hq, num_kv_heads=hkv, head_dim=d, num_blocks=nb)
+        dw = pipeline.DeviceWorkload(wl)
+        sb = pipeline.SubBatch(dw, 0, wl.batch)
+        kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, hq, hkv)
+        fn = lambda: sb.attention(stream=stream)
+        _, avg_ms, _ = _time_launches(fn, max(args.steps, 20), max(args.warmup, 3), stream)
+        avg_us = avg_ms * 1e3
+        rows.append({"prefix": P, "suffix": S, "invocations": B, "q_heads": hq, "kv_heads": hkv,
+                     "head_dim": d, "kernel": attention_kernel_name(wl.batch, wl.max_q_len, hq, hkv, d),
+                     "work_groups": grid, "tail_work_groups": tail, "avg_launch_us": round(avg_us, 2),
+                     "tflops": round(sb.flops / (avg_us * 1e-6) / 1e12, 1)})
+        del dw, sb
+        torch.cuda.empty_cache()
+    gm = math.exp(sum(math.log(r["tflops"]) for r in rows) / len(rows))
+    return {"metric": "prefill-attn TFLOP/s across shapes (geometric mean), 1 MI355X",
+            "value": round(gm, 1), "unit": "TFLOP/s", "n_gpus": 1, "steps": max(args.steps, 20),
+            "warmup": max(args.warmup, 3), "ms_per_step": None, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"{len(rows)} single-agent shapes (prefix, suffix, "
+                                   "invocations, heads, head_dim); see sweep"},
+            "roofline": {"bound": "mfma", "achieved": round(gm, 1), "peak": PEAK_BF16_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(gm / PEAK_BF16_TFLOPS, 4), "traffic": None},
+            "cpu_baseline": None, "sweep": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -436,13 +481,15 @@ def main():
                          "steps let it learn the dispatch cycle")
     ap.add_argument("--component", default="pipeline",
                     choices=("pipeline", "kv_write", "kv_offload", "kv_prefetch", "decode",
-                             "cascade_decode", "control_plane"),
+                             "cascade_decode", "control_plane", "attn_sweep"),
                     help="pipeline (default): the serving step; kv_write / kv_offload / "
                          "kv_prefetch: the write-back scatter, the offload copy and the "
                          "prefetch (with a sweep over 64-4096 blocks) on their own; "
                          "decode / cascade_decode: paged decode attention, per sequence or "
                          "with each agent's anchor read once (use --workload decode_batch); "
-                         "control_plane: the host-side scout on a synthetic agent trace")
+                         "control_plane: the host-side scout on a synthetic agent trace; "
+                         "attn_sweep: prefill attention alone over a grid of prefix / "
+                         "suffix lengths, GQA groups and head dims")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a plain 1 GiB device-to-device copy (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -473,6 +520,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes_read": nbytes, "copy_probe_bytes_written": nbytes,
                           "launches": 5}), flush=True)
+        return
+    if args.component == "attn_sweep":
+        print(json.dumps(bench_attn_sweep(args, dev)), flush=True)
         return
     if args.component != "pipeline":
         print(json.dumps(bench_copy(args, dev)), flush=True)
