@@ -447,6 +447,13 @@ const char *cs_status_string(int status);
  * The pointer stays valid until the thread's next call into the library. */
 const char *cs_last_error(void);
 
+/* Static, NUL-terminated digest of the sources the library was built from
+ * (16 hex digits of a SHA-256 over the names and bytes of the kernel
+ * sources, internal headers and this header, as the package's build step
+ * computes it), or "unknown" for a build that did not define it.  Lets a
+ * caller check that a built library matches the sources beside it. */
+const char *cs_source_digest(void);
+
 #ifdef __cplusplus
 }
 #endif

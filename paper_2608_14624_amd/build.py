@@ -7,6 +7,7 @@ compiles every ``csrc/*.hip`` source (and the host-only ``csrc/*.cpp``) into
 """
 
 import glob
+import hashlib
 import os
 import shutil
 import subprocess
@@ -43,12 +44,37 @@ def run(cmd, verbose):
         raise RuntimeError(f"{os.path.basename(cmd[0])} failed with exit code {res.returncode}")
 
 
+def source_files():
+    """Every file the library is built from: the sources and headers under
+    csrc/ and the public header(s) under include/."""
+    files = []
+    for pattern in ("*.hip", "*.cpp", "*.h"):
+        files += glob.glob(os.path.join(PKG_DIR, "csrc", pattern))
+    files += glob.glob(os.path.join(ROOT, "include", "*.h"))
+    return sorted(files)
+
+
+def source_digest():
+    """First 16 hex digits of a SHA-256 over the names and bytes of
+    source_files(); the build embeds it in the library (cs_source_digest)."""
+    h = hashlib.sha256()
+    for path in source_files():
+        h.update(os.path.relpath(path, ROOT).encode())
+        h.update(b"\0")
+        with open(path, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    return h.hexdigest()[:16]
+
+
 def build(verbose=False):
     """Compile the HIP sources and the host-only C++ into the shared library
     and return its path."""
     sources = sorted(glob.glob(os.path.join(PKG_DIR, "csrc", "*.hip")))
     host_sources = sorted(glob.glob(os.path.join(PKG_DIR, "csrc", "*.cpp")))
     includes = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG_DIR, "csrc")]
+    digest = f'-DCS_SOURCE_DIGEST="{source_digest()}"'
+
     tmp = LIB_PATH + ".tmp"
     with tempfile.TemporaryDirectory(prefix="cachescout_build_") as work:
         # the control plane: plain host C++ built by the host compiler, with no
@@ -67,7 +93,7 @@ def build(verbose=False):
              # MFMA accumulators in arch VGPRs: the softmax rescale then works on
              # them in place instead of copying them out of AGPRs every step
              "-mllvm", "-amdgpu-mfma-vgpr-form",
-             "-Wall", "-Wno-unused-result", *includes,
+             "-Wall", "-Wno-unused-result", *includes, digest,
              # hipcc compiles every input as HIP unless told otherwise
              *sources, "-x", "none", *objects, "-o", tmp], verbose)
     os.replace(tmp, LIB_PATH)

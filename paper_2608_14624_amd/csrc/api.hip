@@ -265,6 +265,11 @@ const char* cs_status_string(int status) {
 
 const char* cs_last_error(void) { return g_last_error; }
 
+#ifndef CS_SOURCE_DIGEST
+#define CS_SOURCE_DIGEST "unknown"
+#endif
+const char* cs_source_digest(void) { return CS_SOURCE_DIGEST; }
+
 int cs_prefill_paged_attn(const void* q, const void* k_pool, const void* v_pool,
                           const int32_t* block_tables, const int32_t* prefix_lens,
                           const int32_t* cu_q_lens, int32_t batch, int32_t total_q,

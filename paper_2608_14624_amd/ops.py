@@ -28,7 +28,8 @@ EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_kv_write", "cs_kv_off
             "cs_scout_score_block", "cs_scout_select_victim", "cs_scout_predictability",
             "cs_scout_between_step", "cs_scout_state_bytes", "cs_scout_set_host_resident",
             "cs_scout_survival_all", "cs_scout_observe_touches", "cs_cascade_decode_attn",
-            "cs_cascade_decode_workspace_bytes", "cs_prefill_paged_attn_launch_shape")
+            "cs_cascade_decode_workspace_bytes", "cs_prefill_paged_attn_launch_shape",
+            "cs_source_digest")
 
 
 class ScoutParams(ctypes.Structure):
@@ -73,6 +74,8 @@ def _load():
     lib.cs_status_string.restype = ctypes.c_char_p
     lib.cs_last_error.argtypes = []
     lib.cs_last_error.restype = ctypes.c_char_p
+    lib.cs_source_digest.argtypes = []
+    lib.cs_source_digest.restype = ctypes.c_char_p
     i64, u64, f64, h = ctypes.c_int64, ctypes.c_uint64, ctypes.c_double, ctypes.c_void_p
     sigs = {
         "cs_scout_default_params": ([ctypes.POINTER(ScoutParams)], None),
@@ -114,6 +117,11 @@ def status_string(status):
 
 def last_error():
     return _lib.cs_last_error().decode()
+
+
+def source_digest():
+    """Digest of the sources the loaded library was built from."""
+    return _lib.cs_source_digest().decode()
 
 
 def _ptr(t):

@@ -34,6 +34,14 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), f"{name} not exported"
 
 
+def test_library_is_built_from_the_sources_beside_it():
+    """A library left over from an earlier edit of the sources would make every
+    GPU test check stale code: the digest the build embeds must match the tree."""
+    from paper_2608_14624_amd import build
+    assert ops.source_digest() == build.source_digest(), (
+        "libcachescout.so is stale: rebuild with python -m paper_2608_14624_amd.build")
+
+
 def test_status_strings():
     assert ops.status_string(0) == "CS_OK"
     assert ops.status_string(1) == "CS_ERR_INVALID_ARG"
