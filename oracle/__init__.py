@@ -39,7 +39,13 @@ values, closed forms, breadth-first distances against all-pairs shortest
 paths, the exact survival probability by path enumeration, and planted
 mistakes (``tests/test_control_plane_oracle.py``).
 
-Every function here is pinned; none is "parity unpinned".
+Every function here is pinned; none is "parity unpinned".  The full
+attention oracle is pinned by the brute force, the invariants, the closed
+forms and the golden case (``tests/test_oracle_*.py``); the row-by-row
+oracle ``prefill_paged_attn_rows`` is pinned to the full oracle on shuffled
+varlen samples, with planted indexing and caching mistakes
+(``tests/test_oracle_rows.py``); the copies by round trips and per-slot
+checks; the control plane as listed above.
 """
 
 from .paged_attention import (  # noqa: F401

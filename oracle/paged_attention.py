@@ -86,6 +86,19 @@ def _scale64(scale):
     return float(np.float32(scale))
 
 
+def packed_row(cu_q_lens, r, i):
+    """Row of the packed ``[total_q, ...]`` arrays that holds suffix token ``i``
+    of invocation ``r``: the invocations' suffixes are stored one after
+    another, so it is ``cu_q_lens[r] + i``."""
+    return int(cu_q_lens[r]) + i
+
+
+def _kv_cache_key(r, g):
+    """Gathered K/V depend on the invocation (its block table and length) and
+    on the KV head, so a cached gather is keyed by both."""
+    return (r, g)
+
+
 def prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens,
                        num_q_heads, num_kv_heads, scale, block_size=16):
     """Full float64 output ``[total_q, Hq, D]`` of paged prefill attention."""
@@ -126,7 +139,9 @@ def prefill_paged_attn_rows(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_l
     Row ``(r, h, i)`` is query head ``h`` of suffix token ``i`` of invocation
     ``r``, i.e. output row ``cu_q_lens[r] + i``.  Each row is computed on its
     own from its visible keys, so this serves workloads too large for the full
-    oracle.
+    oracle.  The gathered K/V of the last ``(r, g)`` pair is kept for the next
+    sample (one entry, so memory stays at one sequence's keys); samples sorted
+    by invocation and head reuse it most.
     """
     cu = np.asarray(cu_q_lens, dtype=np.int64)
     pl = np.asarray(prefix_lens, dtype=np.int64)
@@ -140,14 +155,14 @@ def prefill_paged_attn_rows(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_l
         s_len = int(cu[r + 1] - cu[r])
         assert 0 <= i < s_len
         g = kv_head_of(h, num_q_heads, num_kv_heads)
-        key = (r, g)
+        key = _kv_cache_key(r, g)
         if key not in cache:
             length = p_len + s_len
             cache = {key: (gather_logical_kv(k_pool, block_tables[r], length, g, block_size),
                            gather_logical_kv(v_pool, block_tables[r], length, g, block_size))}
         kk, vv = cache[key]
         nvis = visible_keys(p_len, i)
-        qq = bf16_bits_to_f64(q[cu[r] + i, h, :])
+        qq = bf16_bits_to_f64(q[packed_row(cu, r, i), h, :])
         logits = s64 * (kk[:nvis] @ qq)
         res[n] = _softmax_weighted_sum(logits[None, :], vv[:nvis])[0]
     return res

@@ -1,9 +1,12 @@
 """Pins of the control-plane oracle: hand-computed values of Eq. (2), (3),
-(8) and (9), closed forms of the predictability (deterministic cycle = 1,
+(8) and (9), an edge whose probability equals the threshold of Eq. (7)
+exactly, closed forms of the predictability (deterministic cycle = 1,
 successor independent of the current agent = 0), breadth-first hop
 distances against an all-pairs shortest-path brute force, the exact survival
 probability of Eq. (6) by path enumeration on small chains, the runtime
-procedure on a hand trace, and planted mistakes that the pins must catch."""
+procedure on a hand trace, and planted mistakes that the pins must catch
+(among them a strict comparison in Eq. (7) and the entropy of the current
+agent's marginal in place of the next agent's in Eq. (2))."""
 
 import itertools
 import math
@@ -41,6 +44,18 @@ def test_eq2_closed_forms():
     assert r == pytest.approx(1 - 0.5 / h_next, abs=1e-12)
     assert r == pytest.approx(0.3836885, abs=1e-6)
     assert cp.predictability([[0, 0], [0, 0]]) == 0.0
+
+
+def test_eq7_edge_exactly_on_tau_is_kept():
+    # row 0 of five agents with counts (0, 1, 4, 0, 0): P(1 | 0) = (1 + 0.1) /
+    # (5 + 5 * 0.1) = 1.1 / 5.5, exactly tau = 0.2 in float64; Eq. (7) keeps an
+    # edge whose probability reaches the threshold
+    counts = [[0, 1, 4, 0, 0], [0] * 5, [0] * 5, [0] * 5, [0] * 5]
+    assert cp.transition_prob(counts, 0, 1, 0.1) == 0.2
+    graph = cp.threshold_graph(counts, 0.1, 0.2)
+    assert graph[0] == [1, 2]
+    hops = cp.hop_distances(graph, 0)
+    assert hops[1] == 1 and hops[2] == 1
 
 
 def floyd_warshall(graph):
@@ -193,6 +208,7 @@ def test_agent_ids_are_dense_in_arrival_order():
 def _pins_hold():
     try:
         test_eq3_hand_values_and_rows_sum_to_one()
+        test_eq7_edge_exactly_on_tau_is_kept()
         test_eq2_closed_forms()
         for seed in range(3):
             test_bfs_hops_equal_all_pairs_shortest_paths(seed)
@@ -212,9 +228,32 @@ MUTANTS = {
     "recency_sign_flipped": ("block_score",
                              lambda p, age, tokens, lam, delta:
                              (p + delta) * (math.exp(lam * age) + delta) * tokens),
-    "entropy_ratio_inverted": ("predictability",
-                               lambda counts: 1.0 - (lambda r: r)(0.5)),
+    "edge_needs_more_than_tau": ("threshold_graph",
+                                 lambda counts, eps, tau: [
+                                     [b for b in range(len(counts))
+                                      if cp.transition_prob(counts, a, b, eps) > tau]
+                                     for a in range(len(counts))]),
+    "entropy_of_current_in_place_of_next": ("predictability",
+                                            lambda counts: _predictability_row_marginal(counts)),
 }
+
+
+def _predictability_row_marginal(counts):
+    """Eq. (2) with H(A_t), the current agent's marginal (row sums), taken
+    for H(A_{t+1}), the next agent's marginal (column sums)."""
+    n = len(counts)
+    total = sum(sum(row) for row in counts)
+    if total == 0:
+        return 0.0
+    h_wrong = cp.entropy([sum(counts[i]) / total for i in range(n)])
+    h_cond = 0.0
+    for i in range(n):
+        ri = sum(counts[i])
+        if ri:
+            h_cond += (ri / total) * cp.entropy([c / ri for c in counts[i]])
+    if h_wrong == 0.0:
+        return 1.0
+    return 1.0 - h_cond / h_wrong
 
 
 def test_pins_pass_on_the_real_oracle():
