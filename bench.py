@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "prefill-attn TFLOP/s (% bf16 MFMA peak) + KV prefetch GB/s, 1 MI355X"
 PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
+PEAK_SCLK_MHZ = 2400.0           # the clock that peak is quoted at
 PEAK_HBM_GBS = 8000.0
 PEAK_PCIE5_X16_GBS = 63.0        # PCIe 5.0 x16, one direction, 128b/130b
 KERNEL_SOURCES = ("paper_2608_14624_amd/csrc/prefill_paged_attn.hip",
@@ -97,37 +98,71 @@ def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim)
     return f"prefill_paged_attn_kernel<{head_dim}, false, true>"
 
 
-def cpu_baseline(wl, budget_s=20.0):
-    """The float64 oracle on whole invocations of the same workload, as many as
-    fit the time budget (at least one), in TFLOP/s of algorithmic work."""
+def _oracle_invocations(wl, kp, vp, rs):
+    """Run the float64 oracle on invocations ``rs`` one by one; returns
+    (seconds, algorithmic FLOP)."""
     import numpy as np
     import oracle
+    cu = wl.cu_q_lens.astype(np.int64)
+    flops, t0 = 0, time.perf_counter()
+    for r in rs:
+        s = int(cu[r + 1] - cu[r])
+        p = int(wl.prefix_lens[r])
+        oracle.prefill_paged_attn(wl.q[cu[r]:cu[r + 1]], kp, vp, wl.block_tables[r:r + 1],
+                                  wl.prefix_lens[r:r + 1], np.array([0, s]), wl.num_q_heads,
+                                  wl.num_kv_heads, wl.scale)
+        flops += 4 * wl.head_dim * wl.num_q_heads * (s * p + s * (s + 1) // 2)
+    return time.perf_counter() - t0, flops
+
+
+def cpu_baseline(wl, sample_s=2.0, repeats=3):
+    """The float64 oracle timed on the host, in TFLOP/s of algorithmic work.
+
+    Main figure: whole invocations of the same workload, taken in order until
+    the first pass holds about ``sample_s`` seconds of work (at least one),
+    run ``repeats`` times with all BLAS threads; the median is reported.
+    Beside it, single-thread figures for the tiny and Llama-3-8B-shape
+    configurations (median of 3 and one run)."""
+    import statistics
+    import oracle
+    from paper_2608_14624_amd.workload import make_config
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
+        threadpool_limits = None
         threads = os.cpu_count()
     kp, vp = wl.k_pool, wl.v_pool
     if wl.prefetch_dst is not None:
         kp, vp = oracle.kv_prefetch(wl.host_k, wl.host_v, wl.prefetch_dst, kp, vp)
-    cu = wl.cu_q_lens.astype(np.int64)
-    done_flops, elapsed, n_inv = 0, 0.0, 0
+    rs, first = [], 0.0
     for r in range(wl.batch):
-        s = int(cu[r + 1] - cu[r])
-        p = int(wl.prefix_lens[r])
-        t0 = time.perf_counter()
-        oracle.prefill_paged_attn(wl.q[cu[r]:cu[r + 1]], kp, vp, wl.block_tables[r:r + 1],
-                                  wl.prefix_lens[r:r + 1], np.array([0, s]), wl.num_q_heads,
-                                  wl.num_kv_heads, wl.scale)
-        elapsed += time.perf_counter() - t0
-        done_flops += 4 * wl.head_dim * wl.num_q_heads * (s * p + s * (s + 1) // 2)
-        n_inv += 1
-        if elapsed >= budget_s:
+        dt, _ = _oracle_invocations(wl, kp, vp, [r])
+        rs.append(r)
+        first += dt
+        if first >= sample_s:
             break
-    return {"value": done_flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+    runs = [_oracle_invocations(wl, kp, vp, rs) for _ in range(repeats)]
+    flops = runs[0][1]
+    secs = [t for t, _ in runs]
+    med = statistics.median(secs)
+    single = {}
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            for name, reps in (("tiny", 3), ("llama8b", 1)):
+                w = make_config(name)
+                allr = list(range(w.batch))
+                ts = [_oracle_invocations(w, w.k_pool, w.v_pool, allr) for _ in range(reps)]
+                t1 = statistics.median([t for t, _ in ts])
+                single[name] = {"value": round(ts[0][1] / t1 / 1e12, 6), "unit": "TFLOP/s",
+                                "seconds": round(t1, 3), "runs": reps}
+    return {"value": round(flops / med / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle", "host": host_description(),
-            "sample": f"{n_inv} of {wl.batch} invocations of {wl.name}, full float64 "
-                      f"oracle ({elapsed:.1f} s)"}
+            "runs_s": [round(t, 3) for t in secs],
+            "sample": f"invocations {rs[0]}..{rs[-1]} ({len(rs)} of {wl.batch}) of {wl.name}, "
+                      f"full float64 oracle, median of {repeats} runs "
+                      f"({med:.2f} s each, {int(threads)} BLAS threads)",
+            "single_thread": single}
 
 
 def _time_launches(fn, steps, warmup, stream):
@@ -176,7 +211,100 @@ def host_description():
             blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
     except Exception:  # pragma: no cover
         pass
-    return {"cpu_model": model, "blas": blas, "logical_cpus": os.cpu_count()}
+    lscpu = {}
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            k, _, v = line.partition(":")
+            if k.strip() in ("Model name", "Vendor ID", "CPU family", "Model", "Socket(s)",
+                             "Core(s) per socket", "Thread(s) per core", "CPU(s)",
+                             "CPU max MHz", "Hypervisor vendor"):
+                lscpu[k.strip()] = v.strip()
+    except Exception:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "lscpu": lscpu, "blas": blas, "logical_cpus": os.cpu_count(),
+            "affinity_cpus": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity")
+            else None}
+
+
+def _find_values(obj, want, inner=None):
+    """Numeric ``value`` fields under every key accepted by ``want`` anywhere
+    in a parsed amd-smi JSON document (``key: {inner: {"value": x}}`` when
+    ``inner`` is given, else ``key: {"value": x}``)."""
+    found = []
+    if isinstance(obj, dict):
+        for k, v in obj.items():
+            if want(k) and isinstance(v, dict):
+                leaf = v.get(inner) if inner else v
+                val = leaf.get("value") if isinstance(leaf, dict) else None
+                if isinstance(val, (int, float)):
+                    found.append(float(val))
+            found += _find_values(v, want, inner)
+    elif isinstance(obj, list):
+        for v in obj:
+            found += _find_values(v, want, inner)
+    return found
+
+
+def sample_clock_power(fn, seconds=3.0):
+    """Run ``fn`` back to back for about ``seconds`` while a thread samples the
+    shader clock (mean over the XCDs' gfx clocks) and the socket power with
+    ``amd-smi metric``; returns medians and sample counts, or the reason it
+    could not sample."""
+    import shutil
+    import statistics
+    import subprocess
+    import threading
+    import torch
+    smi = shutil.which("amd-smi") or ("/opt/rocm/bin/amd-smi"
+                                      if os.path.exists("/opt/rocm/bin/amd-smi") else None)
+    if smi is None:
+        return {"error": "amd-smi not found"}
+    clocks, powers, errors = [], [], []
+    stop = threading.Event()
+
+    def poll():
+        while not stop.is_set():
+            try:
+                r = subprocess.run([smi, "metric", "--clock", "--power", "--json"],
+                                   capture_output=True, text=True, timeout=20)
+                doc = json.loads(r.stdout)
+            except Exception as e:  # pragma: no cover
+                errors.append(repr(e)[:200])
+                time.sleep(0.2)
+                continue
+            gfx = _find_values(doc, lambda k: str(k).startswith("gfx_"), inner="clk")
+            pw = _find_values(doc, lambda k: str(k) in ("socket_power", "current_socket_power",
+                                                        "average_socket_power"))
+            if gfx:
+                clocks.append(sum(gfx) / len(gfx))
+            if pw:
+                powers.append(pw[0])
+            if not gfx and not pw:
+                errors.append(r.stdout[:300])
+
+    th = threading.Thread(target=poll, daemon=True)
+    th.start()
+    t0, n = time.perf_counter(), 0
+    while time.perf_counter() - t0 < seconds or (not clocks and n < 100000 and
+                                                  time.perf_counter() - t0 < 4 * seconds):
+        for _ in range(20):
+            fn()
+            n += 1
+        torch.cuda.synchronize()
+    stop.set()
+    th.join(timeout=30)
+    res = {"window_s": round(time.perf_counter() - t0, 2), "steps": n, "samples": len(clocks)}
+    if clocks:
+        res["sclk_mhz_median"] = round(statistics.median(clocks), 1)
+        res["sclk_mhz_min"] = round(min(clocks), 1)
+        res["sclk_mhz_max"] = round(max(clocks), 1)
+    if powers:
+        res["socket_power_w_median"] = round(statistics.median(powers), 1)
+    if errors and not clocks:
+        res["error"] = errors[0]
+    return res
 
 
 def bench_copy(args, dev):
@@ -506,7 +634,7 @@ def main():
 
     import numpy as np
     import torch
-    from paper_2608_14624_amd import pipeline
+    from paper_2608_14624_amd import build, ops, pipeline
     from paper_2608_14624_amd.workload import make_config
 
     dev = torch.device("cuda:0")
@@ -679,8 +807,19 @@ def main():
         "prefetch_policy": None if pipe is None else {
             "name": args.policy, "hits": pipe.hits - hits0, "misses": pipe.misses - misses0},
         "kernel_sha": khash,
+        "library_digest": ops.source_digest(),
+        "source_digest": build.source_digest(),
         "cpu_baseline": None,
     }
+    # the clock the chip holds under this load, sampled over a few seconds of
+    # the same steps after everything above (the timed region is too short
+    # for amd-smi), and the fraction of the peak at that clock
+    clk = sample_clock_power(warm)
+    result["clock"] = clk
+    if clk.get("sclk_mhz_median"):
+        peak_at = PEAK_BF16_TFLOPS * clk["sclk_mhz_median"] / PEAK_SCLK_MHZ
+        result["roofline"]["frac_at_measured_sclk"] = round(achieved / peak_at, 4)
+        result["roofline"]["peak_at_measured_sclk"] = round(peak_at, 1)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(result), flush=True)

@@ -31,8 +31,13 @@
  * Conventions shared by all calls
  *   - Every pointer is caller-owned.  The GPU calls allocate no device or
  *     host memory and keep no state beyond a per-process cache of device
- *     properties; they are reentrant and may run concurrently on different
- *     streams.  The control plane (cs_scout_*, at the end of this file) is
+ *     properties (the compute-unit count of each device, read once, which
+ *     sizes the attention launch); they are reentrant and may run
+ *     concurrently on different streams.
+ *   - The attention launch orders its work-groups for MI355X's 8 XCDs
+ *     (consecutive work-groups dealt round-robin to the XCDs, one L2 each);
+ *     on a part with another XCD count the result is the same, only the L2
+ *     reuse differs.  The control plane (cs_scout_*, at the end of this file) is
  *     host-only and owns the host memory behind its handle.
  *   - Every call enqueues its kernel on `stream` (NULL = the legacy default
  *     stream of the current device) and return without synchronizing.  Device
@@ -116,7 +121,11 @@ enum cs_status {
  *   num_blocks    pool slots.
  *   num_q_heads, num_kv_heads  num_q_heads % num_kv_heads == 0.
  *   head_dim      64 or 128.   block_size  16.
- *   scale         logit scale, finite (typically 1/sqrt(head_dim)).
+ *   scale         logit scale, finite and > 0 (typically 1/sqrt(head_dim));
+ *                 NaN or Inf -> CS_ERR_INVALID_ARG, 0 or negative ->
+ *                 CS_ERR_UNSUPPORTED (the kernels track the running maximum
+ *                 of the unscaled logits, which orders them only for a
+ *                 positive scale).
  *   out           device, bf16 [total_q][num_q_heads][head_dim], 16-byte
  *                 aligned, must not overlap the inputs.
  *   stream        HIP stream.
@@ -138,22 +147,26 @@ int cs_prefill_paged_attn(const void *q, const void *k_pool, const void *v_pool,
  * which kernel a call runs.
  *
  *   *kernel      CS_ATTN_SPLIT: 128-row tiles, each run by 8 waves over two
- *                halves of its keys (launches of fewer than 256 256-row
- *                tiles, one round on the 256 CUs); CS_ATTN_PING_PONG:
+ *                halves of its keys (launches of fewer 256-row tiles than
+ *                compute units, less than one round); CS_ATTN_PING_PONG:
  *                256-row tiles, where the last *tail_work_groups work-groups
  *                run the tiles of a last round at most half full as split
  *                128-row halves.
  *   *grid        work-groups of the launch (0 for a no-op call).
  *   *tail_work_groups  0 unless *kernel is CS_ATTN_PING_PONG.
  *
- * Arguments as in cs_prefill_paged_attn; batch, max_q_len >= 0, head counts
- * positive with num_q_heads % num_kv_heads == 0, else CS_ERR_INVALID_ARG.
- * Output pointers must be non-null.
+ * num_cus: the compute units to size the launch for (256 on MI355X), or 0
+ * for those of the caller's current device (the count cs_prefill_paged_attn
+ * uses; the runtime is then queried once per device, CS_ERR_HIP if it has
+ * no device).  Other arguments as in cs_prefill_paged_attn; batch,
+ * max_q_len, num_cus >= 0, head counts positive with num_q_heads %
+ * num_kv_heads == 0, else CS_ERR_INVALID_ARG.  Output pointers must be
+ * non-null.
  */
 enum { CS_ATTN_SPLIT = 0, CS_ATTN_PING_PONG = 1 };
 int cs_prefill_paged_attn_launch_shape(int32_t batch, int32_t max_q_len, int32_t num_q_heads,
-                                       int32_t num_kv_heads, int32_t *kernel, int64_t *grid,
-                                       int64_t *tail_work_groups);
+                                       int32_t num_kv_heads, int32_t num_cus, int32_t *kernel,
+                                       int64_t *grid, int64_t *tail_work_groups);
 
 /*
  * KV prefetch: copy whole blocks from pinned host memory into pool slots.
@@ -205,6 +218,7 @@ int cs_kv_prefetch(const void *host_k_blocks, const void *host_v_blocks,
  *   block_tables   device, int32 [batch][max_blocks_per_seq].
  *   seq_lens       device, int32 [batch], each in [1, max_seq_len].
  *   num_q_heads / num_kv_heads <= 16; head_dim 64 or 128; block_size 16.
+ *   scale          finite and > 0, as in cs_prefill_paged_attn.
  *   batch == 0 is a no-op returning CS_OK.
  */
 int cs_paged_decode_attn(const void *q, const void *k_pool, const void *v_pool,

@@ -43,7 +43,7 @@ Every function here is pinned; none is "parity unpinned".  The full
 attention oracle is pinned by the brute force, the invariants, the closed
 forms and the golden case (``tests/test_oracle_*.py``); the row-by-row
 oracle ``prefill_paged_attn_rows`` is pinned to the full oracle on shuffled
-varlen samples, with planted indexing and caching mistakes
+varlen samples, with planted indexing and grouping mistakes
 (``tests/test_oracle_rows.py``); the copies by round trips and per-slot
 checks; the control plane as listed above.
 """

@@ -93,9 +93,9 @@ def packed_row(cu_q_lens, r, i):
     return int(cu_q_lens[r]) + i
 
 
-def _kv_cache_key(r, g):
+def _kv_group_key(r, g):
     """Gathered K/V depend on the invocation (its block table and length) and
-    on the KV head, so a cached gather is keyed by both."""
+    on the KV head, so sampled rows share a gather only when both agree."""
     return (r, g)
 
 
@@ -133,36 +133,44 @@ def prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens,
 
 
 def prefill_paged_attn_rows(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens,
-                            num_q_heads, num_kv_heads, scale, samples, block_size=16):
+                            num_q_heads, num_kv_heads, scale, samples, block_size=16,
+                            rows_per_product=1024):
     """Float64 output rows for sampled ``(r, h, i)`` triples, shape ``[n, D]``.
 
     Row ``(r, h, i)`` is query head ``h`` of suffix token ``i`` of invocation
-    ``r``, i.e. output row ``cu_q_lens[r] + i``.  Each row is computed on its
-    own from its visible keys, so this serves workloads too large for the full
-    oracle.  The gathered K/V of the last ``(r, g)`` pair is kept for the next
-    sample (one entry, so memory stays at one sequence's keys); samples sorted
-    by invocation and head reuse it most.
+    ``r``, i.e. output row ``cu_q_lens[r] + i``; it attends over keys
+    ``0 .. P_r + i`` of its invocation (the same definition as
+    ``prefill_paged_attn``), so this serves workloads too large for the full
+    oracle.  The samples are grouped by (invocation, KV head): each group's
+    K/V are gathered once and its rows' logits come from one product with
+    the group's stacked queries (at most ``rows_per_product`` rows at a time),
+    each row masked to its own visible keys.
     """
     cu = np.asarray(cu_q_lens, dtype=np.int64)
     pl = np.asarray(prefix_lens, dtype=np.int64)
     s64 = _scale64(scale)
     d = q.shape[-1]
     res = np.zeros((len(samples), d), dtype=np.float64)
-    cache = {}
+    groups = {}
     for n, (r, h, i) in enumerate(samples):
         r, h, i = int(r), int(h), int(i)
-        p_len = int(pl[r])
-        s_len = int(cu[r + 1] - cu[r])
-        assert 0 <= i < s_len
+        assert 0 <= i < int(cu[r + 1] - cu[r])
         g = kv_head_of(h, num_q_heads, num_kv_heads)
-        key = _kv_cache_key(r, g)
-        if key not in cache:
-            length = p_len + s_len
-            cache = {key: (gather_logical_kv(k_pool, block_tables[r], length, g, block_size),
-                           gather_logical_kv(v_pool, block_tables[r], length, g, block_size))}
-        kk, vv = cache[key]
-        nvis = visible_keys(p_len, i)
-        qq = bf16_bits_to_f64(q[packed_row(cu, r, i), h, :])
-        logits = s64 * (kk[:nvis] @ qq)
-        res[n] = _softmax_weighted_sum(logits[None, :], vv[:nvis])[0]
+        groups.setdefault(_kv_group_key(r, g), []).append((n, r, g, h, i))
+    for members in groups.values():
+        _, r, g, _, _ = members[0]
+        p_len = int(pl[r])
+        length = p_len + int(cu[r + 1] - cu[r])
+        kk = gather_logical_kv(k_pool, block_tables[r], length, g, block_size)
+        vv = gather_logical_kv(v_pool, block_tables[r], length, g, block_size)
+        keys_j = np.arange(length)[None, :]
+        for c0 in range(0, len(members), rows_per_product):
+            part = members[c0:c0 + rows_per_product]
+            qq = bf16_bits_to_f64(np.stack([q[packed_row(cu, r, i), h, :]
+                                            for _, _, _, h, i in part]))
+            nvis = np.array([visible_keys(p_len, i) for _, _, _, _, i in part])[:, None]
+            logits = np.where(keys_j < nvis, s64 * (qq @ kk.T), -np.inf)
+            out = _softmax_weighted_sum(logits, vv)
+            for k, (n, _, _, _, _) in enumerate(part):
+                res[n] = out[k]
     return res

@@ -11,10 +11,15 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
 #include <vector>
 
 namespace {
 thread_local char g_last_error[512];
+
+// compute units per device ordinal, 0 until read
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_device_cus[kMaxDevices];
 }  // namespace
 
 namespace cs {
@@ -30,6 +35,27 @@ int fail(int status, const char* fmt, ...) {
 int ok() {
   g_last_error[0] = '\0';
   return CS_OK;
+}
+
+hipError_t current_device_cus(int* cus) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const bool cached = dev >= 0 && dev < kMaxDevices;
+  if (cached) {
+    const int c = g_device_cus[dev].load(std::memory_order_relaxed);
+    if (c > 0) {
+      *cus = c;
+      return hipSuccess;
+    }
+  }
+  int c = 0;
+  e = hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (c <= 0) return hipErrorInvalidDevice;
+  if (cached) g_device_cus[dev].store(c, std::memory_order_relaxed);
+  *cus = c;
+  return hipSuccess;
 }
 
 }  // namespace cs
@@ -231,6 +257,7 @@ int validate_decode(const void* q, const void* k_pool, const void* v_pool,
     return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
   if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
   if (!isfinite(scale)) return fail(CS_ERR_INVALID_ARG, "scale is not finite");
+  if (!(scale > 0.f)) return fail(CS_ERR_UNSUPPORTED, "scale %g (supported: > 0)", (double)scale);
   if (batch == 0) {
     *noop = true;
     return CS_OK;
@@ -289,6 +316,7 @@ int cs_prefill_paged_attn(const void* q, const void* k_pool, const void* v_pool,
     return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
   if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
   if (!isfinite(scale)) return fail(CS_ERR_INVALID_ARG, "scale is not finite");
+  if (!(scale > 0.f)) return fail(CS_ERR_UNSUPPORTED, "scale %g (supported: > 0)", (double)scale);
   if (batch == 0 || total_q == 0 || max_q_len == 0) return ok();
   if (!q || !k_pool || !v_pool || !block_tables || !prefix_lens || !cu_q_lens || !out)
     return fail(CS_ERR_INVALID_ARG, "null pointer argument");
@@ -298,7 +326,10 @@ int cs_prefill_paged_attn(const void* q, const void* k_pool, const void* v_pool,
     return fail(CS_ERR_INVALID_ARG, "max_blocks_per_seq * block_size < max_kv_len");
   if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
     return fail(CS_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be 16-byte aligned");
-  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, num_q_heads, num_kv_heads);
+  int cus = 0;
+  hipError_t ecu = cs::current_device_cus(&cus);
+  if (ecu != hipSuccess) return hip_fail(ecu, "compute-unit count of the current device");
+  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, num_q_heads, num_kv_heads, cus);
   if (geo.grid > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -322,19 +353,25 @@ int cs_prefill_paged_attn(const void* q, const void* k_pool, const void* v_pool,
   a.num_kv_heads = num_kv_heads;
   a.head_dim = head_dim;
   a.scale = scale;
+  a.cus = cus;
   hipError_t e = cs::launch_prefill_paged_attn(a, s);
   if (e != hipSuccess) return hip_fail(e, "prefill_paged_attn launch");
   return ok();
 }
 
 int cs_prefill_paged_attn_launch_shape(int32_t batch, int32_t max_q_len, int32_t num_q_heads,
-                                       int32_t num_kv_heads, int32_t* kernel, int64_t* grid,
-                                       int64_t* tail_work_groups) {
+                                       int32_t num_kv_heads, int32_t num_cus, int32_t* kernel,
+                                       int64_t* grid, int64_t* tail_work_groups) {
   if (!kernel || !grid || !tail_work_groups) return fail(CS_ERR_INVALID_ARG, "null output pointer");
-  if (batch < 0 || max_q_len < 0) return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (batch < 0 || max_q_len < 0 || num_cus < 0) return fail(CS_ERR_INVALID_ARG, "negative size argument");
   if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0)
     return fail(CS_ERR_INVALID_ARG, "num_q_heads %d, num_kv_heads %d", num_q_heads, num_kv_heads);
-  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, num_q_heads, num_kv_heads);
+  int cus = num_cus;
+  if (cus == 0) {
+    hipError_t e = cs::current_device_cus(&cus);
+    if (e != hipSuccess) return hip_fail(e, "compute-unit count of the current device");
+  }
+  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, num_q_heads, num_kv_heads, cus);
   const bool pp = geo.waves == 8;
   *kernel = pp ? CS_ATTN_PING_PONG : CS_ATTN_SPLIT;
   *grid = (batch == 0 || max_q_len == 0) ? 0 : geo.grid;

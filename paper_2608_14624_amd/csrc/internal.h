@@ -22,7 +22,12 @@ struct AttnLaunch {
   int num_kv_heads;
   int head_dim;
   float scale;
+  int cus;            // compute units of the device (sizes the rounds)
 };
+
+// Compute units of the caller's current device, read from the runtime once
+// per device and cached (a host-only query, safe during stream capture).
+hipError_t current_device_cus(int* cus);
 
 // Launch geometry of the attention kernel (host-side, for tests and tuning).
 struct AttnGeometry {
@@ -37,7 +42,10 @@ struct AttnGeometry {
                       // launches only) runs the half tiles of the last round
 };
 
-AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads);
+// cus: compute units of the device.  The work-group order assumes the
+// dispatcher deals consecutive work-groups round-robin to 8 XCDs (MI355X);
+// any other count of XCDs changes only which L2 serves a tile, not the result.
+AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads, int cus);
 hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream);
 
 struct PrefetchLaunch {

@@ -87,8 +87,6 @@ constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kPPWaves = 8;             // ping-pong kernel: two groups of four waves
 constexpr int kPPThreads = 64 * kPPWaves;
-// CUs of an MI355X: one round of ping-pong (or split) work-groups
-constexpr long long kCUs = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct Params {
@@ -1557,7 +1555,9 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_split_kerne
 
 }  // namespace
 
-AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads) {
+AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads, int cus) {
+  // one round = one ping-pong (or split) work-group per CU
+  const long long kCUs = cus;
   AttnGeometry geo;
   const int group = num_q_heads / num_kv_heads;
   geo.heads_per_wg = (group % 4 == 0) ? 4 : (group % 2 == 0) ? 2 : 1;
@@ -1590,7 +1590,7 @@ AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv
 }
 
 hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
-  const AttnGeometry geo = attn_geometry(a.batch, a.max_q_len, a.num_q_heads, a.num_kv_heads);
+  const AttnGeometry geo = attn_geometry(a.batch, a.max_q_len, a.num_q_heads, a.num_kv_heads, a.cus);
   Params p;
   p.q = a.q;
   p.k_pool = a.k_pool;

@@ -12,7 +12,10 @@ import os
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcachescout.so")
+# CACHESCOUT_LIB names another build of the same library (the host-sanitized
+# one from build_sanitized.py); by default the in-tree build is loaded
+_LIB_PATH = os.environ.get("CACHESCOUT_LIB") or os.path.join(
+    os.path.dirname(os.path.abspath(__file__)), "libcachescout.so")
 
 CS_OK = 0
 CS_ERR_INVALID_ARG = 1
@@ -96,7 +99,7 @@ def _load():
         "cs_scout_set_host_resident": ([h, i32, i32], ctypes.c_int),
         "cs_scout_survival_all": ([h, ctypes.POINTER(f64)], ctypes.c_int),
         "cs_scout_observe_touches": ([h, vp, vp, vp, vp, i32], ctypes.c_int),
-        "cs_prefill_paged_attn_launch_shape": ([i32, i32, i32, i32, ctypes.POINTER(i32),
+        "cs_prefill_paged_attn_launch_shape": ([i32, i32, i32, i32, i32, ctypes.POINTER(i32),
                                                 ctypes.POINTER(i64), ctypes.POINTER(i64)],
                                                ctypes.c_int),
     }
@@ -171,13 +174,14 @@ def _require(cond, msg):
 ATTN_SPLIT, ATTN_PING_PONG = 0, 1
 
 
-def prefill_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads):
+def prefill_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads, num_cus=0):
     """``(kernel, grid, tail_work_groups)`` of a cs_prefill_paged_attn call
-    (host-only): kernel is ATTN_SPLIT or ATTN_PING_PONG."""
+    (host-only): kernel is ATTN_SPLIT or ATTN_PING_PONG.  ``num_cus`` sizes
+    the launch for that many compute units; 0 takes the current device's."""
     kernel, grid, tail = ctypes.c_int32(), ctypes.c_int64(), ctypes.c_int64()
     _check(_lib.cs_prefill_paged_attn_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads,
-                                                   ctypes.byref(kernel), ctypes.byref(grid),
-                                                   ctypes.byref(tail)))
+                                                   num_cus, ctypes.byref(kernel),
+                                                   ctypes.byref(grid), ctypes.byref(tail)))
     return kernel.value, grid.value, tail.value
 
 

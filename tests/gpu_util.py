@@ -22,9 +22,10 @@ def compare_full(got_bits, ref):
     return float(err.max()), float(err.mean())
 
 
-def sample_rows(wl, n_random, seed, edge=True):
+def sample_rows(wl, n_random, seed, edge=True, edge_all_heads=False):
     """(r, h, i) triples: random rows plus, per invocation, its first and last
-    rows and the rows around block and 32-row tile boundaries."""
+    rows and the rows around block and 32-row tile boundaries (for one random
+    query head each, or for every head with ``edge_all_heads``)."""
     rng = np.random.default_rng(seed)
     q_lens = wl.q_lens
     out = set()
@@ -37,7 +38,10 @@ def sample_rows(wl, n_random, seed, edge=True):
             s = int(q_lens[r])
             for i in {0, 1, 15, 16, 31, 32, 63, 64, s // 2, s - 2, s - 1}:
                 if 0 <= i < s:
-                    out.add((r, int(rng.integers(wl.num_q_heads)), i))
+                    if edge_all_heads:
+                        out.update((r, h, i) for h in range(wl.num_q_heads))
+                    else:
+                        out.add((r, int(rng.integers(wl.num_q_heads)), i))
     return sorted(out)
 
 

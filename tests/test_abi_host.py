@@ -73,6 +73,10 @@ def attn(**kw):
     (dict(head_dim=256), ops.CS_ERR_UNSUPPORTED),
     (dict(block_size=32), ops.CS_ERR_UNSUPPORTED),
     (dict(scale=float("nan")), ops.CS_ERR_INVALID_ARG),
+    (dict(scale=float("inf")), ops.CS_ERR_INVALID_ARG),
+    (dict(scale=0.0), ops.CS_ERR_UNSUPPORTED),
+    (dict(scale=-0.0), ops.CS_ERR_UNSUPPORTED),
+    (dict(scale=-0.125), ops.CS_ERR_UNSUPPORTED),
     (dict(q=None), ops.CS_ERR_INVALID_ARG),
     (dict(out=None), ops.CS_ERR_INVALID_ARG),
     (dict(block_tables=None), ops.CS_ERR_INVALID_ARG),
@@ -183,6 +187,9 @@ DGOOD = dict(q=FAKE, k_pool=FAKE, v_pool=FAKE, block_tables=FAKE, seq_lens=FAKE,
     (dict(max_blocks_per_seq=6), ops.CS_ERR_INVALID_ARG),             # 96 < 100
     (dict(max_seq_len=0), ops.CS_ERR_INVALID_ARG),
     (dict(scale=float("inf")), ops.CS_ERR_INVALID_ARG),
+    (dict(scale=0.0), ops.CS_ERR_UNSUPPORTED),
+    (dict(scale=-0.0), ops.CS_ERR_UNSUPPORTED),
+    (dict(scale=-0.125), ops.CS_ERR_UNSUPPORTED),
 ])
 def test_decode_rejects_bad_arguments(kw, status):
     args = dict(DGOOD)
@@ -231,6 +238,8 @@ def test_cascade_workspace_bytes():
     (dict(workspace=FAKE + 8), ops.CS_ERR_INVALID_ARG),
     (dict(workspace_bytes=100), ops.CS_ERR_INVALID_ARG),
     (dict(workspace_bytes=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(scale=0.0), ops.CS_ERR_UNSUPPORTED),
+    (dict(scale=-0.125), ops.CS_ERR_UNSUPPORTED),
 ])
 def test_cascade_rejects_bad_arguments(kw, status):
     args = dict(CGOOD)
@@ -274,11 +283,22 @@ def test_library_exports_only_the_declared_calls():
     (4, 0, 32, 8, (ops.ATTN_SPLIT, 0, 0)),
 ])
 def test_prefill_launch_shape(batch, max_q, hq, hkv, expect):
-    assert ops.prefill_launch_shape(batch, max_q, hq, hkv) == expect
+    assert ops.prefill_launch_shape(batch, max_q, hq, hkv, num_cus=256) == expect
 
 
-@pytest.mark.parametrize("args", [(-1, 64, 8, 2), (1, -1, 8, 2), (1, 64, 0, 2), (1, 64, 8, 3),
-                                  (1, 64, 8, 0)])
+@pytest.mark.parametrize("cus,expect", [
+    # 128 ping-pong tiles: a full round on 128 CUs, under one on 256 or 160
+    (128, (ops.ATTN_PING_PONG, 128, 0)),
+    (160, (ops.ATTN_SPLIT, 256, 0)),
+    (256, (ops.ATTN_SPLIT, 256, 0)),
+    (120, (ops.ATTN_PING_PONG, 120 + 2 * 8, 16)),      # tail of 8 tiles after a round of 120
+])
+def test_prefill_launch_shape_follows_the_cu_count(cus, expect):
+    assert ops.prefill_launch_shape(1, 1024, 32, 8, num_cus=cus) == expect
+
+
+@pytest.mark.parametrize("args", [(-1, 64, 8, 2, 256), (1, -1, 8, 2, 256), (1, 64, 0, 2, 256),
+                                  (1, 64, 8, 3, 256), (1, 64, 8, 0, 256), (1, 64, 8, 2, -1)])
 def test_prefill_launch_shape_rejects_bad_arguments(args):
     with pytest.raises(ops.CacheScoutError) as ei:
         ops.prefill_launch_shape(*args)

@@ -3,16 +3,17 @@
 ``oracle.prefill_paged_attn_rows`` is what the GPU tests check large
 workloads with (sampled rows of the agent batch, the 70B-shape serving step,
 the long mixed load, and every decode and cascade-decode test).  It has its
-own row indexing and a one-entry gather cache, so it is tied here to
+own row indexing and groups its samples by (invocation, KV head) for one
+gather and one product per group, so it is tied here to
 ``oracle.prefill_paged_attn``, which the brute force, the invariants and the
 golden case pin (Sec. 2.1 "Prefix caching": a hit is the last rows of a full
 recompute).  The batch mixes hits and misses, prefixes that are not a
 multiple of the block size, one-token suffixes and GQA groups of 1, 2 and 4;
-the samples are shuffled across invocations and heads so the cache is
-refilled and reused in every order.  Two plausible mistakes planted in the
-row oracle must be caught: the packed row one position early, and the cache
-keyed by the invocation alone (every head of it would then read the first
-head's keys).
+the samples are shuffled across invocations and heads, so every group
+collects rows from all over the sample list.  Two plausible mistakes planted
+in the row oracle must be caught: the packed row one position early, and
+the groups keyed by the invocation alone (every head of it would then read
+the first sampled head's keys).
 """
 
 import numpy as np
@@ -38,13 +39,13 @@ def all_rows_shuffled(wl, seed):
     return [rows[k] for k in order]
 
 
-def rows_error(wl, samples):
+def rows_error(wl, samples, **kw):
     full = oracle.prefill_paged_attn(wl.q, wl.k_pool, wl.v_pool, wl.block_tables,
                                      wl.prefix_lens, wl.cu_q_lens, wl.num_q_heads,
                                      wl.num_kv_heads, wl.scale)
     got = oracle.prefill_paged_attn_rows(wl.q, wl.k_pool, wl.v_pool, wl.block_tables,
                                          wl.prefix_lens, wl.cu_q_lens, wl.num_q_heads,
-                                         wl.num_kv_heads, wl.scale, samples)
+                                         wl.num_kv_heads, wl.scale, samples, **kw)
     want = np.stack([full[int(wl.cu_q_lens[r]) + i, h] for r, h, i in samples])
     return float(np.abs(got - want).max())
 
@@ -62,16 +63,17 @@ def test_rows_equal_the_full_oracle(hq, hkv):
 
 
 def test_rows_sorted_and_repeated_samples():
-    # sorted order (the cache kept across a whole sequence) and repeats
+    # sorted order, repeated rows, and groups split over several products
     wl = varlen_batch(8, 2, seed=32)
     samples = sorted(all_rows_shuffled(wl, seed=1))
     samples = samples + samples[::7]
     assert rows_error(wl, samples) <= 1e-12
+    assert rows_error(wl, samples, rows_per_product=3) <= 1e-12
 
 
 ROW_MUTANTS = {
     "packed_row_one_early": ("packed_row", lambda cu, r, i: int(cu[r]) + i - 1),
-    "cache_keyed_by_invocation": ("_kv_cache_key", lambda r, g: r),
+    "groups_keyed_by_invocation": ("_kv_group_key", lambda r, g: r),
 }
 
 
