@@ -280,6 +280,44 @@ int cs_cascade_decode_attn(const void *q, const void *k_pool, const void *v_pool
                            int32_t head_dim, int32_t block_size, float scale, void *workspace,
                            int64_t workspace_bytes, void *out, cs_stream_t stream);
 
+/*
+ * Cascade decode without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).
+ *
+ * The same operation, arguments, results and kernels as
+ * cs_cascade_decode_attn, minus workspace / workspace_bytes: the partial
+ * results go to a scratch array of CS_NOALLOC_SCRATCH_BYTES bytes that the
+ * library holds in each device's memory from the time it is loaded until the
+ * process ends.  The call allocates nothing (no hipMalloc, no host buffer).
+ *   - A call whose cs_cascade_decode_workspace_bytes(batch, num_q_heads,
+ *     head_dim, max_shared_len, max_rest_len) exceeds
+ *     CS_NOALLOC_SCRATCH_BYTES returns CS_ERR_UNSUPPORTED before anything
+ *     is enqueued (e.g. 128 sequences x 32 query heads at head_dim 128 and
+ *     16 partials per row need 34 MB: use cs_cascade_decode_attn).
+ *   - Every call on a device shares that device's array: calls that may
+ *     overlap on one device (different streams without ordering, or
+ *     different threads) race and give undefined results.  Order them on one
+ *     stream or with events.  Nothing in the array needs to start at zero:
+ *     every partial a call reads is written earlier in the same call.
+ *   - The first call on each device asks the runtime for the array's device
+ *     address once (make that first call outside a stream capture if the
+ *     runtime cannot answer during one); later calls only launch kernels.
+ *   - CS_DEBUG_CHECK is ignored here (its checks copy metadata to host
+ *     buffers).
+ */
+#define CS_NOALLOC_SCRATCH_BYTES (32 * 1024 * 1024)
+int cs_cascade_decode_attn_noalloc(const void *q, const void *k_pool, const void *v_pool,
+                                   const int32_t *block_tables, const int32_t *seq_lens,
+                                   int32_t batch, int32_t max_seq_len,
+                                   int32_t max_blocks_per_seq, int32_t num_blocks,
+                                   const int32_t *cu_groups, const int32_t *shared_lens,
+                                   int32_t num_groups, int32_t max_group_seqs,
+                                   int32_t max_shared_len, int32_t max_rest_len,
+                                   int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                   int32_t block_size, float scale, void *out,
+                                   cs_stream_t stream);
+
 /* Workspace bytes cs_cascade_decode_attn needs:
  * (ceil(max_shared_len / 1024) + ceil(max_rest_len / 1024)) * batch *
  * num_q_heads * (head_dim + 2) * 4; -1 for a negative size or a zero head

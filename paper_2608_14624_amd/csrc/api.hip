@@ -276,6 +276,127 @@ int validate_decode(const void* q, const void* k_pool, const void* v_pool,
 
 }  // namespace
 
+// Device scratch of cs_cascade_decode_attn_noalloc (the cascade's partial
+// results), one array per device for the life of the process.  Host code
+// never passes this name to a kernel: it uses the address the runtime
+// reports for the current device (scratch_address).
+static __device__ __align__(256) unsigned char scratch[CS_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+std::atomic<void*> g_scratch_address[kMaxDevices];
+
+// Device address of `scratch` on the current device, asked of the runtime on
+// the first call on each device and kept.
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* p = g_scratch_address[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_address[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return hipSuccess;
+}
+
+// cs_cascade_decode_attn with the caller's workspace, or (use_scratch) with
+// this device's scratch array, in which case the metadata debug checks,
+// which copy to host buffers, are skipped.
+int cascade_decode(const void* q, const void* k_pool, const void* v_pool,
+                   const int32_t* block_tables, const int32_t* seq_lens, int32_t batch,
+                   int32_t max_seq_len, int32_t max_blocks_per_seq, int32_t num_blocks,
+                   const int32_t* cu_groups, const int32_t* shared_lens, int32_t num_groups,
+                   int32_t max_group_seqs, int32_t max_shared_len, int32_t max_rest_len,
+                   int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                   int32_t block_size, float scale, void* workspace, int64_t workspace_bytes,
+                   bool use_scratch, void* out, cs_stream_t stream) {
+  bool noop;
+  int st0 = validate_decode(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
+                            max_blocks_per_seq, num_blocks, num_q_heads, num_kv_heads, head_dim,
+                            block_size, scale, out, &noop);
+  if (st0 != CS_OK) return st0;
+  if (num_groups < 0 || max_group_seqs < 0 || max_shared_len < 0 || max_rest_len < 0 ||
+      workspace_bytes < 0)
+    return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (noop) return ok();
+  if (num_groups < 1 || num_groups > batch)
+    return fail(CS_ERR_INVALID_ARG, "num_groups %d outside [1, batch = %d]", num_groups, batch);
+  if (max_group_seqs < 1 || max_group_seqs > batch)
+    return fail(CS_ERR_INVALID_ARG, "max_group_seqs %d outside [1, batch = %d]", max_group_seqs, batch);
+  if (max_shared_len > max_seq_len)
+    return fail(CS_ERR_INVALID_ARG, "max_shared_len %d exceeds max_seq_len %d", max_shared_len, max_seq_len);
+  if (max_rest_len > max_seq_len)
+    return fail(CS_ERR_INVALID_ARG, "max_rest_len %d exceeds max_seq_len %d", max_rest_len, max_seq_len);
+  if (!cu_groups || !shared_lens) return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  const int64_t need = cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim, max_shared_len,
+                                                         max_rest_len);
+  if (use_scratch) {
+    if (need > (int64_t)CS_NOALLOC_SCRATCH_BYTES)
+      return fail(CS_ERR_UNSUPPORTED, "this call needs %lld bytes of scratch; the allocation-free "
+                  "entry point holds %lld (use cs_cascade_decode_attn with a workspace)",
+                  (long long)need, (long long)CS_NOALLOC_SCRATCH_BYTES);
+    hipError_t e = scratch_address(&workspace);
+    if (e != hipSuccess) return hip_fail(e, "scratch address on the current device");
+    workspace_bytes = CS_NOALLOC_SCRATCH_BYTES;
+  }
+  if (need > 0) {
+    if (!workspace || !aligned16(workspace))
+      return fail(CS_ERR_INVALID_ARG, "workspace must be a 16-byte aligned device buffer");
+    if (workspace_bytes < need)
+      return fail(CS_ERR_INVALID_ARG, "workspace_bytes %lld < %lld required", (long long)workspace_bytes,
+                  (long long)need);
+  }
+  const cs::CascadeGeometry geo = cs::cascade_geometry(num_groups, max_group_seqs, max_shared_len,
+                                                       max_rest_len, num_q_heads, num_kv_heads);
+  if (geo.grid > 0x7fffffffLL || (long long)batch * num_kv_heads * geo.segments > 0x7fffffffLL)
+    return fail(CS_ERR_INVALID_ARG, "launch too large");
+  if (geo.chunks + geo.segments > cs::kCascadeMaxParts)
+    return fail(CS_ERR_UNSUPPORTED, "%d partials per row (max %d): max_shared_len / 1024 + "
+                "max_rest_len / 1024 too large", geo.chunks + geo.segments, cs::kCascadeMaxParts);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (!use_scratch && debug_checks_enabled()) {
+    int st = debug_check_decode(block_tables, seq_lens, batch, max_seq_len, max_blocks_per_seq,
+                                num_blocks, s);
+    if (st == CS_OK)
+      st = debug_check_groups(block_tables, seq_lens, cu_groups, shared_lens, batch, num_groups,
+                              max_group_seqs, max_shared_len, max_rest_len, max_blocks_per_seq, s);
+    if (st != CS_OK) return st;
+  }
+  cs::CascadeLaunch a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_tables = block_tables;
+  a.seq_lens = seq_lens;
+  a.cu_groups = cu_groups;
+  a.shared_lens = shared_lens;
+  a.out = static_cast<uint16_t*>(out);
+  a.ws_o = static_cast<float*>(workspace);
+  a.ws_ml = a.ws_o + (size_t)(geo.chunks + geo.segments) * batch * num_q_heads * head_dim;
+  a.batch = batch;
+  a.max_blocks_per_seq = max_blocks_per_seq;
+  a.num_groups = num_groups;
+  a.max_group_seqs = max_group_seqs;
+  a.max_shared_len = max_shared_len;
+  a.max_rest_len = max_rest_len;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.scale = scale;
+  hipError_t e = cs::launch_shared_prefix_partials(a, s);
+  if (e != hipSuccess) return hip_fail(e, "shared-prefix attention launch");
+  e = cs::launch_cascade_decode_rest(a, s);
+  if (e != hipSuccess) return hip_fail(e, "cascade decode launch");
+  return ok();
+}
+
+}  // namespace
+
 // the C ABI is the only thing the library exports (built with -fvisibility=hidden)
 #pragma GCC visibility push(default)
 extern "C" {
@@ -474,75 +595,27 @@ int cs_cascade_decode_attn(const void* q, const void* k_pool, const void* v_pool
                            int32_t max_rest_len, int32_t num_q_heads, int32_t num_kv_heads,
                            int32_t head_dim, int32_t block_size, float scale, void* workspace,
                            int64_t workspace_bytes, void* out, cs_stream_t stream) {
-  bool noop;
-  int st0 = validate_decode(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
-                            max_blocks_per_seq, num_blocks, num_q_heads, num_kv_heads, head_dim,
-                            block_size, scale, out, &noop);
-  if (st0 != CS_OK) return st0;
-  if (num_groups < 0 || max_group_seqs < 0 || max_shared_len < 0 || max_rest_len < 0 ||
-      workspace_bytes < 0)
-    return fail(CS_ERR_INVALID_ARG, "negative size argument");
-  if (noop) return ok();
-  if (num_groups < 1 || num_groups > batch)
-    return fail(CS_ERR_INVALID_ARG, "num_groups %d outside [1, batch = %d]", num_groups, batch);
-  if (max_group_seqs < 1 || max_group_seqs > batch)
-    return fail(CS_ERR_INVALID_ARG, "max_group_seqs %d outside [1, batch = %d]", max_group_seqs, batch);
-  if (max_shared_len > max_seq_len)
-    return fail(CS_ERR_INVALID_ARG, "max_shared_len %d exceeds max_seq_len %d", max_shared_len, max_seq_len);
-  if (max_rest_len > max_seq_len)
-    return fail(CS_ERR_INVALID_ARG, "max_rest_len %d exceeds max_seq_len %d", max_rest_len, max_seq_len);
-  if (!cu_groups || !shared_lens) return fail(CS_ERR_INVALID_ARG, "null pointer argument");
-  const int64_t need = cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim, max_shared_len,
-                                                         max_rest_len);
-  if (need > 0) {
-    if (!workspace || !aligned16(workspace))
-      return fail(CS_ERR_INVALID_ARG, "workspace must be a 16-byte aligned device buffer");
-    if (workspace_bytes < need)
-      return fail(CS_ERR_INVALID_ARG, "workspace_bytes %lld < %lld required", (long long)workspace_bytes,
-                  (long long)need);
-  }
-  const cs::CascadeGeometry geo = cs::cascade_geometry(num_groups, max_group_seqs, max_shared_len,
-                                                       max_rest_len, num_q_heads, num_kv_heads);
-  if (geo.grid > 0x7fffffffLL || (long long)batch * num_kv_heads * geo.segments > 0x7fffffffLL)
-    return fail(CS_ERR_INVALID_ARG, "launch too large");
-  if (geo.chunks + geo.segments > cs::kCascadeMaxParts)
-    return fail(CS_ERR_UNSUPPORTED, "%d partials per row (max %d): max_shared_len / 1024 + "
-                "max_rest_len / 1024 too large", geo.chunks + geo.segments, cs::kCascadeMaxParts);
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (debug_checks_enabled()) {
-    int st = debug_check_decode(block_tables, seq_lens, batch, max_seq_len, max_blocks_per_seq,
-                                num_blocks, s);
-    if (st == CS_OK)
-      st = debug_check_groups(block_tables, seq_lens, cu_groups, shared_lens, batch, num_groups,
-                              max_group_seqs, max_shared_len, max_rest_len, max_blocks_per_seq, s);
-    if (st != CS_OK) return st;
-  }
-  cs::CascadeLaunch a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.k_pool = static_cast<const uint16_t*>(k_pool);
-  a.v_pool = static_cast<const uint16_t*>(v_pool);
-  a.block_tables = block_tables;
-  a.seq_lens = seq_lens;
-  a.cu_groups = cu_groups;
-  a.shared_lens = shared_lens;
-  a.out = static_cast<uint16_t*>(out);
-  a.ws_o = static_cast<float*>(workspace);
-  a.ws_ml = a.ws_o + (size_t)(geo.chunks + geo.segments) * batch * num_q_heads * head_dim;
-  a.batch = batch;
-  a.max_blocks_per_seq = max_blocks_per_seq;
-  a.num_groups = num_groups;
-  a.max_group_seqs = max_group_seqs;
-  a.max_shared_len = max_shared_len;
-  a.max_rest_len = max_rest_len;
-  a.num_q_heads = num_q_heads;
-  a.num_kv_heads = num_kv_heads;
-  a.head_dim = head_dim;
-  a.scale = scale;
-  hipError_t e = cs::launch_shared_prefix_partials(a, s);
-  if (e != hipSuccess) return hip_fail(e, "shared-prefix attention launch");
-  e = cs::launch_cascade_decode_rest(a, s);
-  if (e != hipSuccess) return hip_fail(e, "cascade decode launch");
-  return ok();
+  return cascade_decode(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
+                        max_blocks_per_seq, num_blocks, cu_groups, shared_lens, num_groups,
+                        max_group_seqs, max_shared_len, max_rest_len, num_q_heads, num_kv_heads,
+                        head_dim, block_size, scale, workspace, workspace_bytes, false, out,
+                        stream);
+}
+
+int cs_cascade_decode_attn_noalloc(const void* q, const void* k_pool, const void* v_pool,
+                                   const int32_t* block_tables, const int32_t* seq_lens,
+                                   int32_t batch, int32_t max_seq_len,
+                                   int32_t max_blocks_per_seq, int32_t num_blocks,
+                                   const int32_t* cu_groups, const int32_t* shared_lens,
+                                   int32_t num_groups, int32_t max_group_seqs,
+                                   int32_t max_shared_len, int32_t max_rest_len,
+                                   int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                                   int32_t block_size, float scale, void* out,
+                                   cs_stream_t stream) {
+  return cascade_decode(q, k_pool, v_pool, block_tables, seq_lens, batch, max_seq_len,
+                        max_blocks_per_seq, num_blocks, cu_groups, shared_lens, num_groups,
+                        max_group_seqs, max_shared_len, max_rest_len, num_q_heads, num_kv_heads,
+                        head_dim, block_size, scale, nullptr, 0, true, out, stream);
 }
 
 int cs_kv_write(const void* k_new, const void* v_new, const int32_t* slot_mapping,

@@ -32,7 +32,10 @@ EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_kv_write", "cs_kv_off
             "cs_scout_between_step", "cs_scout_state_bytes", "cs_scout_set_host_resident",
             "cs_scout_survival_all", "cs_scout_observe_touches", "cs_cascade_decode_attn",
             "cs_cascade_decode_workspace_bytes", "cs_prefill_paged_attn_launch_shape",
-            "cs_source_digest")
+            "cs_source_digest", "cs_cascade_decode_attn_noalloc")
+
+# bytes of the device scratch array behind cs_cascade_decode_attn_noalloc
+NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024
 
 
 class ScoutParams(ctypes.Structure):
@@ -71,6 +74,10 @@ def _load():
                                            i32, i32, i32, i32, i32, i32, i32, f32, vp,
                                            ctypes.c_int64, vp, vp]
     lib.cs_cascade_decode_attn.restype = ctypes.c_int
+    lib.cs_cascade_decode_attn_noalloc.argtypes = [vp, vp, vp, vp, vp, i32, i32, i32, i32, vp, vp,
+                                                   i32, i32, i32, i32, i32, i32, i32, i32, f32,
+                                                   vp, vp]
+    lib.cs_cascade_decode_attn_noalloc.restype = ctypes.c_int
     lib.cs_cascade_decode_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
     lib.cs_cascade_decode_workspace_bytes.restype = ctypes.c_int64
     lib.cs_status_string.argtypes = [ctypes.c_int]
@@ -399,6 +406,20 @@ def cs_cascade_decode_attn_raw(q, k_pool, v_pool, block_tables, seq_lens, batch,
                                        workspace_bytes, out, stream)
 
 
+def cs_cascade_decode_attn_noalloc_raw(q, k_pool, v_pool, block_tables, seq_lens, batch,
+                                       max_seq_len, max_blocks_per_seq, num_blocks, cu_groups,
+                                       shared_lens, num_groups, max_group_seqs, max_shared_len,
+                                       max_rest_len, num_q_heads, num_kv_heads, head_dim,
+                                       block_size, scale, out, stream=0):
+    """The allocation-free C call with raw pointers (ints or None); returns the status."""
+    return _lib.cs_cascade_decode_attn_noalloc(q, k_pool, v_pool, block_tables, seq_lens, batch,
+                                               max_seq_len, max_blocks_per_seq, num_blocks,
+                                               cu_groups, shared_lens, num_groups,
+                                               max_group_seqs, max_shared_len, max_rest_len,
+                                               num_q_heads, num_kv_heads, head_dim, block_size,
+                                               ctypes.c_float(scale), out, stream)
+
+
 def cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim, max_shared_len, max_rest_len):
     return int(_lib.cs_cascade_decode_workspace_bytes(batch, num_q_heads, head_dim,
                                                       max_shared_len, max_rest_len))
@@ -441,6 +462,37 @@ def cs_cascade_decode_attn(q, k_pool, v_pool, block_tables, seq_lens, cu_groups,
         float(scale),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(out),
         _stream_handle(stream, dev)))
+
+
+def cs_cascade_decode_attn_noalloc(q, k_pool, v_pool, block_tables, seq_lens, cu_groups,
+                                   shared_lens, out, *, max_seq_len, max_group_seqs,
+                                   max_shared_len, max_rest_len, scale, stream=None):
+    """Enqueue cascade decode attention with the partials in the library's
+    per-device scratch array (no workspace, nothing allocated; calls on one
+    device must not overlap).  Tensors as for :func:`cs_cascade_decode_attn`."""
+    dev = q.device
+    for name, t, dt in (("q", q, torch.bfloat16), ("k_pool", k_pool, torch.bfloat16),
+                        ("v_pool", v_pool, torch.bfloat16), ("out", out, torch.bfloat16),
+                        ("block_tables", block_tables, torch.int32),
+                        ("seq_lens", seq_lens, torch.int32), ("cu_groups", cu_groups, torch.int32),
+                        ("shared_lens", shared_lens, torch.int32)):
+        _require(t.is_cuda and t.device == dev, f"{name} must be on {dev}")
+        _require(t.dtype == dt, f"{name} must be {dt}")
+        _require(t.is_contiguous(), f"{name} must be contiguous")
+    _require(q.dim() == 3 and out.shape == q.shape, "q and out must be [B, Hq, D]")
+    _require(k_pool.shape == v_pool.shape and k_pool.dim() == 4, "pools must match")
+    batch, hq, d = q.shape
+    num_blocks, hkv, bs, d2 = k_pool.shape
+    _require(d == d2, "head_dim of q and pools differ")
+    _require(block_tables.dim() == 2 and block_tables.shape[0] == batch, "block_tables must be [B, max_blocks]")
+    _require(seq_lens.numel() == batch, "seq_lens must have B entries")
+    num_groups = shared_lens.numel()
+    _require(cu_groups.numel() == num_groups + 1, "cu_groups must have G + 1 entries")
+    _check(cs_cascade_decode_attn_noalloc_raw(
+        _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_tables), _ptr(seq_lens), batch,
+        int(max_seq_len), block_tables.shape[1], num_blocks, _ptr(cu_groups), _ptr(shared_lens),
+        num_groups, int(max_group_seqs), int(max_shared_len), int(max_rest_len), hq, hkv, d, bs,
+        float(scale), _ptr(out), _stream_handle(stream, dev)))
 
 
 def scout_default_params():

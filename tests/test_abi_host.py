@@ -303,3 +303,38 @@ def test_prefill_launch_shape_rejects_bad_arguments(args):
     with pytest.raises(ops.CacheScoutError) as ei:
         ops.prefill_launch_shape(*args)
     assert ei.value.args[0].startswith("CS_ERR_INVALID_ARG")
+
+
+def cascade_noalloc(**kw):
+    args = {k: v for k, v in CGOOD.items() if k not in ("workspace", "workspace_bytes")}
+    args.update(kw)
+    return ops.cs_cascade_decode_attn_noalloc_raw(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(head_dim=96), ops.CS_ERR_UNSUPPORTED),
+    (dict(num_groups=0), ops.CS_ERR_INVALID_ARG),
+    (dict(cu_groups=None), ops.CS_ERR_INVALID_ARG),
+    (dict(scale=0.0), ops.CS_ERR_UNSUPPORTED),
+    # 128 sequences x 32 heads x (D + 2) x 4 B x (8 + 8) partials = 34 MB > 32 MiB
+    (dict(batch=128, num_q_heads=32, num_kv_heads=8, max_seq_len=16384, max_blocks_per_seq=1024,
+          num_groups=8, max_group_seqs=16, max_shared_len=8192, max_rest_len=8192),
+     ops.CS_ERR_UNSUPPORTED),
+])
+def test_cascade_noalloc_rejects_bad_arguments_before_any_gpu_call(kw, status):
+    assert cascade_noalloc(**kw) == status
+    if status == ops.CS_ERR_UNSUPPORTED and kw.get("batch") == 128:
+        need = ops.cs_cascade_decode_workspace_bytes(128, 32, 128, 8192, 8192)
+        assert need > ops.NOALLOC_SCRATCH_BYTES
+        assert "scratch" in ops.last_error()
+
+
+def test_cascade_noalloc_empty_batch_is_a_noop():
+    assert cascade_noalloc(batch=0, q=None, num_groups=0) == ops.CS_OK
+
+
+def test_noalloc_scratch_size_matches_the_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define CS_NOALLOC_SCRATCH_BYTES \((\d+) \* (\d+) \* (\d+)\)", text)
+    assert m and int(m[1]) * int(m[2]) * int(m[3]) == ops.NOALLOC_SCRATCH_BYTES
