@@ -595,6 +595,61 @@ def bench_attn_sweep(args, dev):
             "cpu_baseline": None, "sweep": rows}
 
 
+def bench_kv_locality(args, dev):
+    """What the K/V fetches cost the prefill attention: the workload's batch in
+    one launch with its real block tables, then the same launch (same
+    lengths, the same FLOP) with every table entry pointing at one of 16 pool
+    slots of the first invocation, so that every K/V read after the first
+    few hits in L2.  The difference bounds what any scheme that reads each
+    shared anchor block only once (a shared-prefix cascade) can save; the
+    cascade's own partial results would add HBM traffic on top."""
+    import numpy as np
+    import torch
+    from paper_2608_14624_amd import ops, pipeline
+    from paper_2608_14624_amd.workload import make_config
+    stream = torch.cuda.current_stream(dev)
+    wl = make_config(args.workload)
+    dw = pipeline.DeviceWorkload(wl)
+    dw.prefetch_all()
+    sb = pipeline.SubBatch(dw, 0, wl.batch)
+    steps, warm = max(args.steps, 20), max(args.warmup, 3)
+    _, real_ms, real_list = _time_launches(lambda: sb.attention(stream=stream), steps, warm, stream)
+    n0 = -(-int(wl.kv_lens[0]) // wl.block_size)
+    hot = wl.block_tables[0, :min(16, n0)].astype(np.int32)
+    bt_hot = hot[np.arange(wl.block_tables.shape[1]) % len(hot)][None, :].repeat(wl.batch, axis=0)
+    bt_hot_d = torch.from_numpy(np.ascontiguousarray(bt_hot)).to(dev)
+    out_hot = torch.empty_like(dw.out)
+
+    def hot_call():
+        ops.cs_prefill_paged_attn(dw.q, dw.k_pool, dw.v_pool, bt_hot_d, dw.prefix_lens,
+                                  dw.cu_q_lens, out_hot, max_q_len=wl.max_q_len,
+                                  max_kv_len=wl.max_kv_len, scale=wl.scale, stream=stream)
+    _, hot_ms, hot_list = _time_launches(hot_call, steps, warm, stream)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out_hot.float()).all().item()
+    flops = wl.flops()
+    rows = wl.total_q * wl.num_q_heads
+    # a cascade writes and reads back two fp32 partials (O, m, l) per row:
+    # the shared-anchor part and the own-key part
+    partial_bytes = 2 * 2 * rows * (wl.head_dim + 2) * 4
+    real_us, hot_us = real_ms * 1e3, hot_ms * 1e3
+    return {"metric": "prefill-attn us per launch, real block tables vs K/V served from L2",
+            "value": round(real_us, 2), "unit": "us", "n_gpus": 1, "steps": steps,
+            "warmup": warm, "ms_per_step": round(real_ms, 4), "higher_is_better": False,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"{args.workload}: {DESCRIPTIONS.get(args.workload, '')}",
+                       "launch": "all invocations in one cs_prefill_paged_attn call",
+                       "hot_slots": int(len(hot))},
+            "real_tables": {"avg_launch_us": round(real_us, 2), "launch_us": percentiles_us(real_list),
+                            "tflops": round(flops / (real_ms * 1e-3) / 1e12, 1)},
+            "kv_from_l2": {"avg_launch_us": round(hot_us, 2), "launch_us": percentiles_us(hot_list),
+                           "tflops": round(flops / (hot_ms * 1e-3) / 1e12, 1)},
+            "kv_fetch_share_of_time": round(1.0 - hot_us / real_us, 4),
+            "cascade_partial_bytes": partial_bytes,
+            "cascade_partial_us_at_5tbs": round(partial_bytes / 5e12 * 1e6, 1),
+            "roofline": None, "cpu_baseline": None}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -609,7 +664,7 @@ def main():
                          "steps let it learn the dispatch cycle")
     ap.add_argument("--component", default="pipeline",
                     choices=("pipeline", "kv_write", "kv_offload", "kv_prefetch", "decode",
-                             "cascade_decode", "control_plane", "attn_sweep"),
+                             "cascade_decode", "control_plane", "attn_sweep", "kv_locality"),
                     help="pipeline (default): the serving step; kv_write / kv_offload / "
                          "kv_prefetch: the write-back scatter, the offload copy and the "
                          "prefetch (with a sweep over 64-4096 blocks) on their own; "
@@ -617,7 +672,9 @@ def main():
                          "with each agent's anchor read once (use --workload decode_batch); "
                          "control_plane: the host-side scout on a synthetic agent trace; "
                          "attn_sweep: prefill attention alone over a grid of prefix / "
-                         "suffix lengths, GQA groups and head dims")
+                         "suffix lengths, GQA groups and head dims; kv_locality: one "
+                         "launch of the workload with its real block tables and with every "
+                         "K/V read served from L2 (what a shared-prefix cascade could save)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a plain 1 GiB device-to-device copy (the reference kernel "
                          "for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE readings)")
@@ -651,6 +708,9 @@ def main():
         return
     if args.component == "attn_sweep":
         print(json.dumps(bench_attn_sweep(args, dev)), flush=True)
+        return
+    if args.component == "kv_locality":
+        print(json.dumps(bench_kv_locality(args, dev)), flush=True)
         return
     if args.component != "pipeline":
         print(json.dumps(bench_copy(args, dev)), flush=True)
