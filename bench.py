@@ -84,10 +84,14 @@ def load_traffic(kernel, workload, kernel_hash):
     return entry.get("bytes_per_launch")
 
 
-def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim):
+def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim, parts=1):
     """Which attention kernel a launch runs (the library's own launch rule,
-    asked through cs_prefill_paged_attn_launch_shape)."""
+    asked through cs_prefill_paged_attn_launch_shape; ``parts`` > 1: the
+    workspace call's key parts and their merge)."""
     from paper_2608_14624_amd import ops
+    if parts > 1:
+        return (f"prefill_paged_attn_ppd_split_kernel<{head_dim}, true> + "
+                f"prefill_split_merge_kernel<{head_dim}>")
     kernel, _, tail = ops.prefill_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads)
     if kernel == ops.ATTN_PING_PONG:
         if head_dim == 128:
@@ -96,6 +100,16 @@ def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim)
     if head_dim == 128:
         return "prefill_paged_attn_ppd_split_kernel<128>"
     return f"prefill_paged_attn_kernel<{head_dim}, false, true>"
+
+
+def key_parts(sb, wl, workspace):
+    """Key parts the attention call of sub-batch ``sb`` takes (1: none)."""
+    from paper_2608_14624_amd import ops
+    if workspace is None or sb.hi <= sb.lo:
+        return 1
+    need = ops.prefill_workspace_bytes(sb.hi - sb.lo, sb.q1 - sb.q0, sb.max_q_len, sb.max_kv_len,
+                                       wl.num_q_heads, wl.num_kv_heads, wl.head_dim)
+    return max(1, need // ((sb.q1 - sb.q0) * wl.num_q_heads * (wl.head_dim + 2) * 4))
 
 
 def _oracle_invocations(wl, kp, vp, rs):
@@ -658,6 +672,10 @@ def main():
     ap.add_argument("--workload", default="llama70b_prefetch",
                     choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-workspace", action="store_true",
+                    help="run the plain cs_prefill_paged_attn; by default the attention runs "
+                         "cs_prefill_paged_attn_ws, which splits launches too small to fill the "
+                         "GPU into key parts (launches of a round or more are unchanged)")
     ap.add_argument("--policy", default="order", choices=("order", "scout"),
                     help="prefetch target: the next agent in dispatch order (default) or the "
                          "control plane's between-step decision (cs_scout_*); the warmup "
@@ -716,7 +734,7 @@ def main():
         print(json.dumps(bench_copy(args, dev)), flush=True)
         return
     wl = make_config(args.workload)
-    dw = pipeline.DeviceWorkload(wl, dev)
+    dw = pipeline.DeviceWorkload(wl, dev, workspace=None if args.no_workspace else "auto")
     main_stream = torch.cuda.current_stream(dev)
     if wl.prefetch_dst is not None:
         # serving order with the next agent's prefetch overlapped on a side stream
@@ -826,13 +844,11 @@ def main():
                         "serial_sum_ms_per_step": round(alone_step_ms + iso * n_launch, 4),
                         "overlapped_ms_per_step": round(ms_per_step, 4)}}
     khash = source_hash(KERNEL_SOURCES[:1])
-    if pipe is not None:
-        kernel_names = sorted({attention_kernel_name(b.hi - b.lo, b.max_q_len, wl.num_q_heads,
-                                                     wl.num_kv_heads, wl.head_dim)
-                               for b in pipe.batches})
-    else:
-        kernel_names = [attention_kernel_name(wl.batch, wl.max_q_len, wl.num_q_heads,
-                                              wl.num_kv_heads, wl.head_dim)]
+    batches = pipe.batches if pipe is not None else [pipeline.SubBatch(dw, 0, wl.batch)]
+    kernel_names = sorted({attention_kernel_name(b.hi - b.lo, b.max_q_len, wl.num_q_heads,
+                                                 wl.num_kv_heads, wl.head_dim,
+                                                 key_parts(b, wl, dw.workspace))
+                           for b in batches})
     kernel_name = " + ".join(kernel_names)
     traffic = load_traffic(kernel_name, args.workload, khash)
     result = {

@@ -142,6 +142,49 @@ int cs_prefill_paged_attn(const void *q, const void *k_pool, const void *v_pool,
                           cs_stream_t stream);
 
 /*
+ * The same attention with a caller workspace, for launches too small to fill
+ * the device (Sec. 2.1 "Prefix caching", as cs_prefill_paged_attn).
+ *
+ * When a call of cs_prefill_paged_attn would run its split kernel on at most
+ * half as many 128-row tiles as there are compute units, this call cuts
+ * every tile's key steps into `parts` contiguous pieces (2 to 4: as many as
+ * fit one round of one work-group per CU, at most half the key steps of the
+ * longest sequence) that run on separate work-groups; each writes its rows'
+ * partial result (O relative to its running maximum m, m, and the
+ * probability sum l, in fp32) to the workspace, and a second kernel combines
+ * the parts of every (token, query head) row with log-sum-exp weights into
+ * the bf16 output.  The result equals cs_prefill_paged_attn's up to rounding
+ * order.  Other launches (head_dim 64, more tiles) ignore the workspace and
+ * run exactly as cs_prefill_paged_attn.
+ *
+ * Arguments as in cs_prefill_paged_attn, plus
+ *   workspace        device, 16-byte aligned, caller-owned scratch of at least
+ *                    cs_prefill_paged_attn_workspace_bytes(batch, total_q,
+ *                    max_q_len, max_kv_len, num_q_heads, num_kv_heads,
+ *                    head_dim, 0) bytes (may be NULL when that is 0); its
+ *                    contents are undefined after the call; calls that share
+ *                    a workspace must be ordered on one stream.
+ *   workspace_bytes  its size; smaller than required -> CS_ERR_INVALID_ARG.
+ */
+int cs_prefill_paged_attn_ws(const void *q, const void *k_pool, const void *v_pool,
+                             const int32_t *block_tables, const int32_t *prefix_lens,
+                             const int32_t *cu_q_lens, int32_t batch, int32_t total_q,
+                             int32_t max_q_len, int32_t max_kv_len, int32_t max_blocks_per_seq,
+                             int32_t num_blocks, int32_t num_q_heads, int32_t num_kv_heads,
+                             int32_t head_dim, int32_t block_size, float scale, void *workspace,
+                             int64_t workspace_bytes, void *out, cs_stream_t stream);
+
+/* Workspace bytes cs_prefill_paged_attn_ws needs: parts * total_q *
+ * num_q_heads * (head_dim + 2) * 4, or 0 when the launch takes no key parts.
+ * num_cus: compute units to size for, 0 = the current device's (-1 if there
+ * is none).  -1 for a negative size, bad head counts or a head_dim other
+ * than 64 or 128. */
+int64_t cs_prefill_paged_attn_workspace_bytes(int32_t batch, int32_t total_q, int32_t max_q_len,
+                                              int32_t max_kv_len, int32_t num_q_heads,
+                                              int32_t num_kv_heads, int32_t head_dim,
+                                              int32_t num_cus);
+
+/*
  * Launch shape of cs_prefill_paged_attn for a batch: a host-only query (no
  * GPU work, no device pointers) for profilers and tests that need to know
  * which kernel a call runs.

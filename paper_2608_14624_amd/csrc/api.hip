@@ -276,6 +276,95 @@ int validate_decode(const void* q, const void* k_pool, const void* v_pool,
 
 }  // namespace
 
+namespace {
+
+// Workspace bytes of a launch with key parts: per part, an fp32 O row and
+// (m, l) for every (token, query head); 0 without parts.
+int64_t key_part_bytes(const cs::AttnGeometry& geo, int32_t total_q, int32_t num_q_heads,
+                       int32_t head_dim) {
+  if (geo.parts <= 1) return 0;
+  return (int64_t)geo.parts * total_q * num_q_heads * (head_dim + 2) * (int64_t)sizeof(float);
+}
+
+// cs_prefill_paged_attn, and with a workspace (has_ws) the variant whose
+// launches that would leave CUs idle split their keys into parts
+int prefill_paged_attn(const void* q, const void* k_pool, const void* v_pool,
+                       const int32_t* block_tables, const int32_t* prefix_lens,
+                       const int32_t* cu_q_lens, int32_t batch, int32_t total_q, int32_t max_q_len,
+                       int32_t max_kv_len, int32_t max_blocks_per_seq, int32_t num_blocks,
+                       int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                       int32_t block_size, float scale, bool has_ws, void* workspace,
+                       int64_t workspace_bytes, void* out, cs_stream_t stream) {
+  if (batch < 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0 || max_blocks_per_seq < 0 ||
+      num_blocks < 0)
+    return fail(CS_ERR_INVALID_ARG, "negative size argument");
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
+    return fail(CS_ERR_INVALID_ARG, "head counts, head_dim and block_size must be positive");
+  if (num_q_heads % num_kv_heads != 0)
+    return fail(CS_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                num_q_heads, num_kv_heads);
+  if (head_dim != 64 && head_dim != 128)
+    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
+  if (!isfinite(scale)) return fail(CS_ERR_INVALID_ARG, "scale is not finite");
+  if (!(scale > 0.f)) return fail(CS_ERR_UNSUPPORTED, "scale %g (supported: > 0)", (double)scale);
+  if (batch == 0 || total_q == 0 || max_q_len == 0) return ok();
+  if (!q || !k_pool || !v_pool || !block_tables || !prefix_lens || !cu_q_lens || !out)
+    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
+  if (num_blocks == 0) return fail(CS_ERR_INVALID_ARG, "num_blocks is 0");
+  if (max_q_len > max_kv_len) return fail(CS_ERR_INVALID_ARG, "max_q_len exceeds max_kv_len");
+  if ((long long)max_blocks_per_seq * block_size < max_kv_len)
+    return fail(CS_ERR_INVALID_ARG, "max_blocks_per_seq * block_size < max_kv_len");
+  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
+    return fail(CS_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be 16-byte aligned");
+  if (has_ws && workspace_bytes < 0) return fail(CS_ERR_INVALID_ARG, "negative workspace_bytes");
+  int cus = 0;
+  hipError_t ecu = cs::current_device_cus(&cus);
+  if (ecu != hipSuccess) return hip_fail(ecu, "compute-unit count of the current device");
+  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, max_kv_len, num_q_heads,
+                                                 num_kv_heads, head_dim, cus, has_ws);
+  if (geo.grid > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
+  const int64_t need = key_part_bytes(geo, total_q, num_q_heads, head_dim);
+  if (need > 0) {
+    if (!workspace || !aligned16(workspace))
+      return fail(CS_ERR_INVALID_ARG, "workspace must be a 16-byte aligned device buffer");
+    if (workspace_bytes < need)
+      return fail(CS_ERR_INVALID_ARG, "workspace_bytes %lld < %lld required", (long long)workspace_bytes,
+                  (long long)need);
+  }
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (debug_checks_enabled()) {
+    int st = debug_check_attn(block_tables, prefix_lens, cu_q_lens, batch, total_q, max_q_len,
+                              max_kv_len, max_blocks_per_seq, num_blocks, s);
+    if (st != CS_OK) return st;
+  }
+  cs::AttnLaunch a;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_tables = block_tables;
+  a.prefix_lens = prefix_lens;
+  a.cu_q_lens = cu_q_lens;
+  a.out = static_cast<uint16_t*>(out);
+  a.batch = batch;
+  a.max_q_len = max_q_len;
+  a.max_blocks_per_seq = max_blocks_per_seq;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = num_kv_heads;
+  a.head_dim = head_dim;
+  a.scale = scale;
+  a.cus = cus;
+  a.max_kv_len = max_kv_len;
+  a.total_q = total_q;
+  a.workspace = need > 0 ? workspace : nullptr;
+  hipError_t e = cs::launch_prefill_paged_attn(a, s);
+  if (e != hipSuccess) return hip_fail(e, "prefill_paged_attn launch");
+  return ok();
+}
+
+}  // namespace
+
 // Device scratch of cs_cascade_decode_attn_noalloc (the cascade's partial
 // results), one array per device for the life of the process.  Host code
 // never passes this name to a kernel: it uses the address the runtime
@@ -425,59 +514,38 @@ int cs_prefill_paged_attn(const void* q, const void* k_pool, const void* v_pool,
                           int32_t num_blocks, int32_t num_q_heads, int32_t num_kv_heads,
                           int32_t head_dim, int32_t block_size, float scale, void* out,
                           cs_stream_t stream) {
-  if (batch < 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0 || max_blocks_per_seq < 0 ||
-      num_blocks < 0)
-    return fail(CS_ERR_INVALID_ARG, "negative size argument");
-  if (num_q_heads <= 0 || num_kv_heads <= 0 || head_dim <= 0 || block_size <= 0)
-    return fail(CS_ERR_INVALID_ARG, "head counts, head_dim and block_size must be positive");
-  if (num_q_heads % num_kv_heads != 0)
-    return fail(CS_ERR_INVALID_ARG, "num_q_heads %d is not a multiple of num_kv_heads %d",
-                num_q_heads, num_kv_heads);
-  if (head_dim != 64 && head_dim != 128)
-    return fail(CS_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", head_dim);
-  if (block_size != 16) return fail(CS_ERR_UNSUPPORTED, "block_size %d (supported: 16)", block_size);
-  if (!isfinite(scale)) return fail(CS_ERR_INVALID_ARG, "scale is not finite");
-  if (!(scale > 0.f)) return fail(CS_ERR_UNSUPPORTED, "scale %g (supported: > 0)", (double)scale);
-  if (batch == 0 || total_q == 0 || max_q_len == 0) return ok();
-  if (!q || !k_pool || !v_pool || !block_tables || !prefix_lens || !cu_q_lens || !out)
-    return fail(CS_ERR_INVALID_ARG, "null pointer argument");
-  if (num_blocks == 0) return fail(CS_ERR_INVALID_ARG, "num_blocks is 0");
-  if (max_q_len > max_kv_len) return fail(CS_ERR_INVALID_ARG, "max_q_len exceeds max_kv_len");
-  if ((long long)max_blocks_per_seq * block_size < max_kv_len)
-    return fail(CS_ERR_INVALID_ARG, "max_blocks_per_seq * block_size < max_kv_len");
-  if (!aligned16(q) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
-    return fail(CS_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be 16-byte aligned");
-  int cus = 0;
-  hipError_t ecu = cs::current_device_cus(&cus);
-  if (ecu != hipSuccess) return hip_fail(ecu, "compute-unit count of the current device");
-  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, num_q_heads, num_kv_heads, cus);
-  if (geo.grid > 0x7fffffffLL) return fail(CS_ERR_INVALID_ARG, "launch too large");
+  return prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, batch, total_q,
+                            max_q_len, max_kv_len, max_blocks_per_seq, num_blocks, num_q_heads,
+                            num_kv_heads, head_dim, block_size, scale, false, nullptr, 0, out, stream);
+}
 
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (debug_checks_enabled()) {
-    int st = debug_check_attn(block_tables, prefix_lens, cu_q_lens, batch, total_q, max_q_len,
-                              max_kv_len, max_blocks_per_seq, num_blocks, s);
-    if (st != CS_OK) return st;
-  }
-  cs::AttnLaunch a;
-  a.q = static_cast<const uint16_t*>(q);
-  a.k_pool = static_cast<const uint16_t*>(k_pool);
-  a.v_pool = static_cast<const uint16_t*>(v_pool);
-  a.block_tables = block_tables;
-  a.prefix_lens = prefix_lens;
-  a.cu_q_lens = cu_q_lens;
-  a.out = static_cast<uint16_t*>(out);
-  a.batch = batch;
-  a.max_q_len = max_q_len;
-  a.max_blocks_per_seq = max_blocks_per_seq;
-  a.num_q_heads = num_q_heads;
-  a.num_kv_heads = num_kv_heads;
-  a.head_dim = head_dim;
-  a.scale = scale;
-  a.cus = cus;
-  hipError_t e = cs::launch_prefill_paged_attn(a, s);
-  if (e != hipSuccess) return hip_fail(e, "prefill_paged_attn launch");
-  return ok();
+int cs_prefill_paged_attn_ws(const void* q, const void* k_pool, const void* v_pool,
+                             const int32_t* block_tables, const int32_t* prefix_lens,
+                             const int32_t* cu_q_lens, int32_t batch, int32_t total_q,
+                             int32_t max_q_len, int32_t max_kv_len, int32_t max_blocks_per_seq,
+                             int32_t num_blocks, int32_t num_q_heads, int32_t num_kv_heads,
+                             int32_t head_dim, int32_t block_size, float scale, void* workspace,
+                             int64_t workspace_bytes, void* out, cs_stream_t stream) {
+  return prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, batch, total_q,
+                            max_q_len, max_kv_len, max_blocks_per_seq, num_blocks, num_q_heads,
+                            num_kv_heads, head_dim, block_size, scale, true, workspace,
+                            workspace_bytes, out, stream);
+}
+
+int64_t cs_prefill_paged_attn_workspace_bytes(int32_t batch, int32_t total_q, int32_t max_q_len,
+                                              int32_t max_kv_len, int32_t num_q_heads,
+                                              int32_t num_kv_heads, int32_t head_dim,
+                                              int32_t num_cus) {
+  if (batch < 0 || total_q < 0 || max_q_len < 0 || max_kv_len < 0 || num_cus < 0 ||
+      num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0 ||
+      (head_dim != 64 && head_dim != 128))
+    return -1;
+  if (batch == 0 || total_q == 0 || max_q_len == 0) return 0;
+  int cus = num_cus;
+  if (cus == 0 && cs::current_device_cus(&cus) != hipSuccess) return -1;
+  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, max_kv_len, num_q_heads,
+                                                 num_kv_heads, head_dim, cus, true);
+  return key_part_bytes(geo, total_q, num_q_heads, head_dim);
 }
 
 int cs_prefill_paged_attn_launch_shape(int32_t batch, int32_t max_q_len, int32_t num_q_heads,
@@ -492,7 +560,8 @@ int cs_prefill_paged_attn_launch_shape(int32_t batch, int32_t max_q_len, int32_t
     hipError_t e = cs::current_device_cus(&cus);
     if (e != hipSuccess) return hip_fail(e, "compute-unit count of the current device");
   }
-  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, num_q_heads, num_kv_heads, cus);
+  const cs::AttnGeometry geo = cs::attn_geometry(batch, max_q_len, max_q_len, num_q_heads, num_kv_heads,
+                                                 128, cus, false);
   const bool pp = geo.waves == 8;
   *kernel = pp ? CS_ATTN_PING_PONG : CS_ATTN_SPLIT;
   *grid = (batch == 0 || max_q_len == 0) ? 0 : geo.grid;

@@ -23,7 +23,13 @@ struct AttnLaunch {
   int head_dim;
   float scale;
   int cus;            // compute units of the device (sizes the rounds)
+  int max_kv_len;
+  int total_q;
+  void* workspace;    // null: no key parts (see attn_geometry)
 };
+
+// most key parts a split launch takes (work-groups per tile)
+constexpr int kMaxKeyParts = 4;
 
 // Compute units of the caller's current device, read from the runtime once
 // per device and cached (a host-only query, safe during stream capture).
@@ -40,12 +46,19 @@ struct AttnGeometry {
   long long grid;     // work-groups launched
   long long pp_grid;  // ping-pong work-groups; the rest of the grid (ping-pong
                       // launches only) runs the half tiles of the last round
+  int parts;          // key parts per split tile (1: none; then grid = tiles)
+  long long split_tiles;  // split launches: tiles per key part
 };
 
 // cus: compute units of the device.  The work-group order assumes the
 // dispatcher deals consecutive work-groups round-robin to 8 XCDs (MI355X);
 // any other count of XCDs changes only which L2 serves a tile, not the result.
-AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads, int cus);
+// allow_parts: the caller gave a workspace, so a split launch that would
+// leave at least half the CUs idle takes its tiles' keys in up to
+// kMaxKeyParts parts on separate work-groups (head_dim 128), whose partials
+// a merge kernel combines.
+AttnGeometry attn_geometry(int batch, int max_q_len, int max_kv_len, int num_q_heads, int num_kv_heads,
+                           int head_dim, int cus, bool allow_parts);
 hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream);
 
 struct PrefetchLaunch {

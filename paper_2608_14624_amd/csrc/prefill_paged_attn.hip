@@ -68,6 +68,7 @@
 
 #include <math.h>
 
+#include <algorithm>
 #include <type_traits>
 
 namespace cs {
@@ -120,6 +121,12 @@ struct Params {
   float* ws_o;                  // [chunks][batch * num_q_heads][D] partial O
   float* ws_ml;                 // [chunks][batch * num_q_heads][2] partial (m, l)
   int ws_rows;                  // batch * num_q_heads
+  // split launches with key parts (partial results in a workspace): work-group
+  // wg takes key part wg / split_tiles of tile wg % split_tiles; the partials
+  // go to ws_o / ws_ml as [parts][total_q * num_q_heads][D] and [..][2]
+  int parts;
+  int split_tiles;
+  long long part_rows;          // total_q * num_q_heads
 };
 
 template <int D>
@@ -939,7 +946,7 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
 // ahead (an iteration takes about 2 us, ample for a load), and the halves
 // merge through LDS at the end.  The arithmetic is that of the split path of
 // the four-wave kernel, in the same order.
-template <int D, bool kTailTile>
+template <int D, bool kTailTile, bool kPartial = false>
 __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, uint16_t* k0, uint16_t* k1,
                                                uint16_t* k2, uint16_t* k3, uint16_t* v0, uint16_t* v1,
                                                uint16_t* v2, uint16_t* v3) {
@@ -960,6 +967,11 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   int tile = wg;
   int sub_half = 0;
   int span = p.span;
+  int part = 0;
+  if constexpr (kPartial) {
+    part = wg / p.split_tiles;
+    tile = wg - part * p.split_tiles;
+  }
   if constexpr (kTailTile) {
     const long long jt = wg - p.pp_grid;
     const int kvh = (int)(jt % p.num_kv_heads);
@@ -987,9 +999,17 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   const int qpos = row_valid ? P + t : L - 1;               // last visible key
   const int kv_end = P + min(S, t0 + span);                 // keys the tile needs
   const int n_all = (kv_end + kBN - 1) / kBN;
-  const int n_iter = n_all - n_all / 2;                     // both halves run as many iterations
-  const int j0 = split_half ? n_all / 2 : 0;
-  const int n_steps = split_half ? n_all - n_all / 2 : n_all / 2;
+  // this work-group's key steps [s0, s1): all of them, or one of p.parts
+  // contiguous parts (a part may be empty)
+  int s0 = 0, s1 = n_all;
+  if constexpr (kPartial) {
+    s0 = (int)((long long)n_all * part / p.parts);
+    s1 = (int)((long long)n_all * (part + 1) / p.parts);
+  }
+  const int n_part = s1 - s0;
+  const int n_iter = n_part - n_part / 2;                   // both halves run as many iterations
+  const int j0 = s0 + (split_half ? n_part / 2 : 0);
+  const int n_steps = split_half ? n_part - n_part / 2 : n_part / 2;
   const int n_blk = (L + kBlock - 1) / kBlock;
   const int32_t* bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
   const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
@@ -1208,6 +1228,23 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
 #pragma unroll
     for (int rr = 0; rr < 16; ++rr) oacc[dt][rr] = w0 * oacc[dt][rr] + w1 * x[(dt * 16 + rr) * 64 + lane];
   l_tot = w0 * l_tot + w1 * l1;
+  if constexpr (kPartial) {
+    // partial result of this key part: O relative to mx, mx and l (a row
+    // whose keys in this part are all masked stores O = 0, -inf, 0)
+    if (row_valid) {
+      const size_t prow = (size_t)part * p.part_rows + (size_t)(q0 + t) * p.num_q_heads + h;
+      float* orow = p.ws_o + prow * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg)
+          *reinterpret_cast<float4*>(orow + dt * 32 + 8 * rg + 4 * half) =
+              make_float4(oacc[dt][rg * 4], oacc[dt][rg * 4 + 1], oacc[dt][rg * 4 + 2], oacc[dt][rg * 4 + 3]);
+      }
+      if (half == 0) *reinterpret_cast<float2*>(p.ws_ml + 2 * prow) = make_float2(mx, l_tot);
+    }
+    return;
+  }
   const float inv = 1.f / l_tot;
   if (row_valid) {
     uint16_t* orow = p.out + qrow;
@@ -1544,21 +1581,61 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
 
 // Launches of less than one round of ping-pong tiles, D = 128: split tiles
 // (128 rows x 8 waves over two halves of the keys) with direct-to-LDS staging.
-template <int D>
+template <int D, bool kPartial>
 __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_split_kernel(Params p) {
   static_assert(D == 128, "direct-to-LDS staging is laid out for 256-byte rows");
   constexpr int kBuf = 16 * (4 * D + 8);
   __shared__ __attribute__((aligned(16))) uint16_t k0[kBuf], k1[kBuf], k2[kBuf], k3[kBuf];
   __shared__ __attribute__((aligned(16))) uint16_t v0[kBuf], v1[kBuf], v2[kBuf], v3[kBuf];
-  ppd_split_tile<D, false>(p, blockIdx.x, k0, k1, k2, k3, v0, v1, v2, v3);
+  ppd_split_tile<D, false, kPartial>(p, blockIdx.x, k0, k1, k2, k3, v0, v1, v2, v3);
+}
+
+// The output of a split launch with key parts: each (token, head) row
+// combines its parts' partial results with the log-sum-exp weights in base
+// 2 (the kernels' own units): w_p = 2^{(m_p - max m) c}, out = sum_p w_p O_p /
+// sum_p w_p l_p, rounded to bf16.  Part 0 holds key 0, which every row sees,
+// so the sum of weights is never empty.  D / 4 threads per row, four
+// consecutive features each.
+template <int D>
+__global__ __launch_bounds__(kThreads) void prefill_split_merge_kernel(Params p) {
+  constexpr int kTpr = D / 4;
+  constexpr int kRowsPerBlock = kThreads / kTpr;
+  const long long row = (long long)blockIdx.x * kRowsPerBlock + threadIdx.x / kTpr;
+  if (row >= p.part_rows) return;
+  const int d0 = (threadIdx.x % kTpr) * 4;
+  const float c = p.scale_log2;
+  float mx = -INFINITY;
+  for (int q = 0; q < p.parts; ++q) mx = fmaxf(mx, p.ws_ml[2 * ((size_t)q * p.part_rows + row)]);
+  float den = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int q = 0; q < p.parts; ++q) {
+    const size_t prow = (size_t)q * p.part_rows + row;
+    const float2 ml = *reinterpret_cast<const float2*>(p.ws_ml + 2 * prow);
+    const float w = ml.x == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((ml.x - mx) * c);
+    const float4 o = *reinterpret_cast<const float4*>(p.ws_o + prow * D + d0);
+    den += w * ml.y;
+    acc.x += w * o.x;
+    acc.y += w * o.y;
+    acc.z += w * o.z;
+    acc.w += w * o.w;
+  }
+  const float inv = 1.f / den;
+  bf16x4 r;
+  r[0] = (__bf16)(acc.x * inv);
+  r[1] = (__bf16)(acc.y * inv);
+  r[2] = (__bf16)(acc.z * inv);
+  r[3] = (__bf16)(acc.w * inv);
+  *reinterpret_cast<uint2*>(p.out + row * D + d0) = __builtin_bit_cast(uint2, r);
 }
 
 }  // namespace
 
-AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv_heads, int cus) {
+AttnGeometry attn_geometry(int batch, int max_q_len, int max_kv_len, int num_q_heads, int num_kv_heads,
+                           int head_dim, int cus, bool allow_parts) {
   // one round = one ping-pong (or split) work-group per CU
   const long long kCUs = cus;
   AttnGeometry geo;
+  geo.parts = 1;
   const int group = num_q_heads / num_kv_heads;
   geo.heads_per_wg = (group % 4 == 0) ? 4 : (group % 2 == 0) ? 2 : 1;
   geo.head_tiles = num_q_heads / geo.heads_per_wg;
@@ -1576,6 +1653,23 @@ AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv
     geo.token_tiles = (max_q_len + geo.span - 1) / geo.span;
     geo.grid = (long long)geo.token_tiles * batch * geo.head_tiles;
     geo.pp_grid = 0;
+    geo.split_tiles = geo.grid;
+    // with a workspace (D = 128), a launch that leaves at least half the CUs
+    // idle cuts each tile's keys into parts on separate work-groups, as many
+    // as fit one round (at most kMaxKeyParts), each part at least two steps
+    // of the longest sequence so that both key halves of a part have work.
+    // (Choosing the parts by the rounds they take, so that launches of more
+    // than half a round split too, was slower: a part's fixed costs of Q
+    // loads, pipeline fill, half merge and partial store outweigh it.)
+    if (allow_parts && head_dim == 128 && geo.grid > 0) {
+      const long long steps = ((long long)max_kv_len + kBN - 1) / kBN;
+      long long parts = std::min<long long>(kCUs / geo.grid, kMaxKeyParts);
+      parts = std::min<long long>(parts, steps / 2);
+      if (parts > 1) {
+        geo.parts = (int)parts;
+        geo.grid *= parts;
+      }
+    }
     return geo;
   }
   // a last round at most half full runs as split half tiles (whose pairs
@@ -1590,7 +1684,8 @@ AttnGeometry attn_geometry(int batch, int max_q_len, int num_q_heads, int num_kv
 }
 
 hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
-  const AttnGeometry geo = attn_geometry(a.batch, a.max_q_len, a.num_q_heads, a.num_kv_heads, a.cus);
+  const AttnGeometry geo = attn_geometry(a.batch, a.max_q_len, a.max_kv_len, a.num_q_heads, a.num_kv_heads,
+                                         a.head_dim, a.cus, a.workspace != nullptr);
   Params p;
   p.q = a.q;
   p.k_pool = a.k_pool;
@@ -1610,7 +1705,20 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
   p.head_tiles = geo.head_tiles;
   p.scale_log2 = a.scale * kLog2e;
   p.pp_grid = geo.pp_grid;
+  p.parts = geo.parts;
+  p.split_tiles = (int)geo.split_tiles;
+  p.part_rows = (long long)a.total_q * a.num_q_heads;
+  p.ws_o = static_cast<float*>(a.workspace);
+  p.ws_ml = p.ws_o ? p.ws_o + (size_t)geo.parts * p.part_rows * a.head_dim : nullptr;
   const dim3 grid((unsigned)geo.grid);
+  if (geo.parts > 1) {
+    // key parts on more work-groups, then the merge of their partials
+    hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<128, true>), grid, dim3(kPPThreads), 0, stream, p);
+    const long long rows_per_block = kThreads / (128 / 4);
+    const dim3 mgrid((unsigned)((p.part_rows + rows_per_block - 1) / rows_per_block));
+    hipLaunchKernelGGL(prefill_split_merge_kernel<128>, mgrid, dim3(kThreads), 0, stream, p);
+    return hipGetLastError();
+  }
   if (geo.waves == kPPWaves) {
     const bool tail = geo.grid > geo.pp_grid;
     if (a.head_dim == 128) {
@@ -1627,7 +1735,7 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
   } else if (a.head_dim == 128) {
     // fewer than one ping-pong work-group per CU: 128-row tiles, each run
     // by 8 waves over two halves of its keys
-    hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<128>), grid, dim3(kPPThreads), 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<128, false>), grid, dim3(kPPThreads), 0, stream, p);
   } else {
     hipLaunchKernelGGL((prefill_paged_attn_kernel<64, false, true>), grid, dim3(2 * kThreads), 0, stream, p);
   }

@@ -32,7 +32,8 @@ EXPORTED = ("cs_prefill_paged_attn", "cs_kv_prefetch", "cs_kv_write", "cs_kv_off
             "cs_scout_between_step", "cs_scout_state_bytes", "cs_scout_set_host_resident",
             "cs_scout_survival_all", "cs_scout_observe_touches", "cs_cascade_decode_attn",
             "cs_cascade_decode_workspace_bytes", "cs_prefill_paged_attn_launch_shape",
-            "cs_source_digest", "cs_cascade_decode_attn_noalloc")
+            "cs_source_digest", "cs_cascade_decode_attn_noalloc", "cs_prefill_paged_attn_ws",
+            "cs_prefill_paged_attn_workspace_bytes")
 
 # bytes of the device scratch array behind cs_cascade_decode_attn_noalloc
 NOALLOC_SCRATCH_BYTES = 32 * 1024 * 1024
@@ -61,6 +62,11 @@ def _load():
     lib.cs_prefill_paged_attn.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
                                           i32, i32, i32, i32, f32, vp, vp]
     lib.cs_prefill_paged_attn.restype = ctypes.c_int
+    lib.cs_prefill_paged_attn_ws.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32,
+                                             i32, i32, i32, i32, f32, vp, ctypes.c_int64, vp, vp]
+    lib.cs_prefill_paged_attn_ws.restype = ctypes.c_int
+    lib.cs_prefill_paged_attn_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32]
+    lib.cs_prefill_paged_attn_workspace_bytes.restype = ctypes.c_int64
     lib.cs_kv_prefetch.argtypes = [vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp]
     lib.cs_kv_prefetch.restype = ctypes.c_int
     lib.cs_kv_write.argtypes = [vp, vp, vp, i32, vp, vp, i32, i32, i32, i32, vp]
@@ -192,16 +198,31 @@ def prefill_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads, num_cus=0)
     return kernel.value, grid.value, tail.value
 
 
-def cs_prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out, *,
-                          max_q_len, max_kv_len, scale, stream=None):
-    """Enqueue paged prefill attention on ``stream`` (default: the current stream).
+def cs_prefill_paged_attn_ws_raw(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, batch,
+                                 total_q, max_q_len, max_kv_len, max_blocks_per_seq, num_blocks,
+                                 num_q_heads, num_kv_heads, head_dim, block_size, scale, workspace,
+                                 workspace_bytes, out, stream=0):
+    """The C call with a workspace, raw pointers (ints or None); returns the status code."""
+    return _lib.cs_prefill_paged_attn_ws(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens,
+                                         batch, total_q, max_q_len, max_kv_len, max_blocks_per_seq,
+                                         num_blocks, num_q_heads, num_kv_heads, head_dim,
+                                         block_size, ctypes.c_float(scale), workspace,
+                                         workspace_bytes, out, stream)
 
-    Tensors: ``q``/``out`` bf16 ``[total_q, Hq, D]``; pools bf16
-    ``[num_blocks, Hkv, 16, D]``; ``block_tables`` int32 ``[B, max_blocks]``;
-    ``prefix_lens`` int32 ``[B]``; ``cu_q_lens`` int32 ``[B+1]``; all on the
-    same GPU and contiguous.  ``max_q_len``/``max_kv_len`` are host integers
-    bounding the suffix and total lengths.
-    """
+
+def prefill_workspace_bytes(batch, total_q, max_q_len, max_kv_len, num_q_heads, num_kv_heads,
+                            head_dim, num_cus=0):
+    """Bytes of workspace ``cs_prefill_paged_attn_ws`` takes (0: the launch
+    does not split its keys into parts)."""
+    return int(_lib.cs_prefill_paged_attn_workspace_bytes(batch, total_q, max_q_len, max_kv_len,
+                                                          num_q_heads, num_kv_heads, head_dim,
+                                                          num_cus))
+
+
+def _prefill_args(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out, max_q_len,
+                  max_kv_len, scale):
+    """Validate a prefill attention call's tensors; the C arguments up to the
+    scale, the output pointer and the device."""
     dev = q.device
     for name, t, dt in (("q", q, torch.bfloat16), ("k_pool", k_pool, torch.bfloat16),
                         ("v_pool", v_pool, torch.bfloat16), ("out", out, torch.bfloat16),
@@ -221,54 +242,79 @@ def cs_prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_len
     batch = block_tables.shape[0]
     _require(prefix_lens.numel() == batch and cu_q_lens.numel() == batch + 1,
              "prefix_lens must have B entries and cu_q_lens B + 1")
-    status = cs_prefill_paged_attn_raw(
-        _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_tables), _ptr(prefix_lens),
-        _ptr(cu_q_lens), batch, total_q, int(max_q_len), int(max_kv_len),
-        block_tables.shape[1], num_blocks, hq, hkv, d, bs, float(scale), _ptr(out),
-        _stream_handle(stream, dev))
-    _check(status)
+    args = (_ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_tables), _ptr(prefix_lens),
+            _ptr(cu_q_lens), batch, total_q, int(max_q_len), int(max_kv_len),
+            block_tables.shape[1], num_blocks, hq, hkv, d, bs, ctypes.c_float(scale))
+    return args, _ptr(out), dev
+
+
+def _resolve_workspace(workspace, args, dev):
+    """None: the call without a workspace.  "auto": a new uint8 GPU tensor of
+    the size the call needs (None if it needs none).  A tensor: used as is."""
+    if workspace is None or (isinstance(workspace, str) and workspace == "auto"):
+        if workspace is None:
+            return None
+        batch, total_q, max_q, max_kv = args[6], args[7], args[8], args[9]
+        hq, hkv, d = args[12], args[13], args[14]
+        need = prefill_workspace_bytes(batch, total_q, max_q, max_kv, hq, hkv, d)
+        _require(need >= 0, "no workspace size for these arguments")
+        if need == 0:
+            return None
+        return torch.empty(need, dtype=torch.uint8, device=dev)
+    _require(workspace.is_cuda and workspace.device == dev, f"workspace must be on {dev}")
+    return workspace
+
+
+def cs_prefill_paged_attn(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out, *,
+                          max_q_len, max_kv_len, scale, workspace=None, stream=None):
+    """Enqueue paged prefill attention on ``stream`` (default: the current stream).
+
+    Tensors: ``q``/``out`` bf16 ``[total_q, Hq, D]``; pools bf16
+    ``[num_blocks, Hkv, 16, D]``; ``block_tables`` int32 ``[B, max_blocks]``;
+    ``prefix_lens`` int32 ``[B]``; ``cu_q_lens`` int32 ``[B+1]``; all on the
+    same GPU and contiguous.  ``max_q_len``/``max_kv_len`` are host integers
+    bounding the suffix and total lengths.  ``workspace``: None (the plain
+    call), "auto" (``cs_prefill_paged_attn_ws`` with a workspace allocated
+    here when the launch splits its keys), or a uint8 GPU tensor for it.
+    """
+    args, outp, dev = _prefill_args(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out,
+                                    max_q_len, max_kv_len, scale)
+    ws = _resolve_workspace(workspace, args, dev)
+    handle = _stream_handle(stream, dev)
+    if workspace is None:
+        _check(_lib.cs_prefill_paged_attn(*args, outp, handle))
+    else:
+        _check(_lib.cs_prefill_paged_attn_ws(*args, _ptr(ws),
+                                             0 if ws is None else ws.numel(), outp, handle))
 
 
 class PrefillCall:
-    """A cs_prefill_paged_attn call with its tensors validated once.
+    """A prefill attention call with its tensors validated once.
 
     Serving loops launch the same attention over the same buffers again and
     again; this keeps the argument checks and pointer extraction out of the
     per-launch path, so each launch costs one C call.  The tensors must stay
-    alive and unchanged in shape while the object is used.
+    alive and unchanged in shape while the object is used.  ``workspace`` as
+    for :func:`cs_prefill_paged_attn` ("auto" allocates it once, here).
     """
 
     def __init__(self, q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out, *,
-                 max_q_len, max_kv_len, scale):
-        # the same checks as cs_prefill_paged_attn, done once
-        dev = q.device
-        for name, t, dt in (("q", q, torch.bfloat16), ("k_pool", k_pool, torch.bfloat16),
-                            ("v_pool", v_pool, torch.bfloat16), ("out", out, torch.bfloat16),
-                            ("block_tables", block_tables, torch.int32),
-                            ("prefix_lens", prefix_lens, torch.int32),
-                            ("cu_q_lens", cu_q_lens, torch.int32)):
-            _require(t.device == dev and t.is_cuda, f"{name} must be on {dev}")
-            _require(t.dtype == dt, f"{name} must be {dt}")
-            _require(t.is_contiguous(), f"{name} must be contiguous")
-        _require(q.dim() == 3 and out.shape == q.shape, "q and out must be [total_q, Hq, D]")
-        _require(k_pool.dim() == 4 and v_pool.shape == k_pool.shape,
-                 "pools must be [num_blocks, Hkv, block_size, D]")
-        _require(block_tables.dim() == 2, "block_tables must be [B, max_blocks]")
-        total_q, hq, d = q.shape
-        num_blocks, hkv, bs, d2 = k_pool.shape
-        _require(d == d2, "head_dim of q and pools differ")
-        batch = block_tables.shape[0]
-        _require(prefix_lens.numel() == batch and cu_q_lens.numel() == batch + 1,
-                 "prefix_lens must have B entries and cu_q_lens B + 1")
+                 max_q_len, max_kv_len, scale, workspace=None):
+        args, outp, dev = _prefill_args(q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens,
+                                        out, max_q_len, max_kv_len, scale)
         self.device = dev
+        self.workspace = _resolve_workspace(workspace, args, dev)
         self._keep = (q, k_pool, v_pool, block_tables, prefix_lens, cu_q_lens, out)
-        self._args = (_ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_tables), _ptr(prefix_lens),
-                      _ptr(cu_q_lens), batch, total_q, int(max_q_len), int(max_kv_len),
-                      block_tables.shape[1], num_blocks, hq, hkv, d, bs, ctypes.c_float(scale),
-                      _ptr(out))
+        if workspace is None:
+            self._fn = _lib.cs_prefill_paged_attn
+            self._args = args + (outp,)
+        else:
+            ws = self.workspace
+            self._fn = _lib.cs_prefill_paged_attn_ws
+            self._args = args + (_ptr(ws), 0 if ws is None else ws.numel(), outp)
 
     def __call__(self, stream=None):
-        _check(_lib.cs_prefill_paged_attn(*self._args, _stream_handle(stream, self.device)))
+        _check(self._fn(*self._args, _stream_handle(stream, self.device)))
 
 
 def cs_kv_prefetch(host_k, host_v, dst_block_ids, k_pool, v_pool, *, stream=None):

@@ -69,7 +69,7 @@ class SubBatch:
             self._call = ops.PrefillCall(self.q, dw.k_pool, dw.v_pool, self.block_tables,
                                          self.prefix_lens, self.cu_q_lens, self.out,
                                          max_q_len=self.max_q_len, max_kv_len=self.max_kv_len,
-                                         scale=wl.scale)
+                                         scale=wl.scale, workspace=dw.workspace)
 
     def attention(self, stream=None):
         if self._call is not None:
@@ -79,8 +79,12 @@ class SubBatch:
 class DeviceWorkload:
     """GPU copies of a :class:`~paper_2608_14624_amd.workload.Workload`."""
 
-    def __init__(self, wl, device="cuda:0"):
+    def __init__(self, wl, device="cuda:0", workspace=None):
+        """``workspace``: None for the plain attention call, "auto" for the
+        call with a workspace (allocated per launch shape when it splits
+        small launches' keys over more work-groups)."""
         self.wl = wl
+        self.workspace = workspace
         self.device = torch.device(device)
         self.q = _to_device_bf16(wl.q, self.device)
         self.k_pool = _to_device_bf16(wl.k_pool, self.device)
@@ -92,7 +96,7 @@ class DeviceWorkload:
         self._call = ops.PrefillCall(self.q, self.k_pool, self.v_pool, self.block_tables,
                                      self.prefix_lens, self.cu_q_lens, self.out,
                                      max_q_len=wl.max_q_len, max_kv_len=wl.max_kv_len,
-                                     scale=wl.scale)
+                                     scale=wl.scale, workspace=workspace)
         self.host_k = self.host_v = self.prefetch_dst = None
         if wl.prefetch_dst is not None:
             self.host_k = _to_pinned_bf16(wl.host_k)
@@ -107,7 +111,7 @@ class DeviceWorkload:
         ops.cs_prefill_paged_attn(self.q, self.k_pool, self.v_pool, self.block_tables,
                                   self.prefix_lens, self.cu_q_lens, out,
                                   max_q_len=wl.max_q_len, max_kv_len=wl.max_kv_len,
-                                  scale=wl.scale, stream=stream)
+                                  scale=wl.scale, workspace=self.workspace, stream=stream)
 
     def prefetch_all(self, stream=None):
         if self.prefetch_dst is None:

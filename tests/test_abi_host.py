@@ -338,3 +338,44 @@ def test_noalloc_scratch_size_matches_the_header():
     text = open(HEADER).read()
     m = re.search(r"#define CS_NOALLOC_SCRATCH_BYTES \((\d+) \* (\d+) \* (\d+)\)", text)
     assert m and int(m[1]) * int(m[2]) * int(m[3]) == ops.NOALLOC_SCRATCH_BYTES
+
+
+@pytest.mark.parametrize("args,expect", [
+    # one GPU's shard of a 70B-shape agent launch: 4 x 512 tokens, 8 / 1 heads:
+    # 128 split tiles on 256 CUs -> 2 key parts of fp32 (D + 2) per row
+    ((4, 2048, 512, 4608, 8, 1, 128, 256), 2 * 2048 * 8 * 130 * 4),
+    # 8 tiles -> 4 parts (the cap)
+    ((1, 100, 100, 1000, 8, 2, 128, 256), 4 * 100 * 8 * 130 * 4),
+    # 3 parts when 85 tiles (4 heads x 32 tokens) leave room for three
+    ((1, 2720, 2720, 2720, 4, 1, 128, 256), 3 * 2720 * 4 * 130 * 4),
+    ((1, 1024, 1024, 3072, 32, 8, 128, 256), 0),        # a full round of tiles: no parts
+    ((1, 100, 100, 1000, 8, 2, 64, 256), 0),            # head_dim 64: no parts
+    ((1, 100, 100, 100, 8, 2, 128, 256), 0),            # two key steps: no parts
+    ((0, 0, 0, 0, 8, 2, 128, 256), 0),
+    ((-1, 100, 100, 1000, 8, 2, 128, 256), -1),
+    ((1, 100, 100, 1000, 8, 3, 128, 256), -1),
+    ((1, 100, 100, 1000, 8, 2, 96, 256), -1),
+])
+def test_prefill_workspace_bytes(args, expect):
+    assert ops.prefill_workspace_bytes(*args) == expect
+
+
+def attn_ws(**kw):
+    args = dict(GOOD, workspace=FAKE, workspace_bytes=1 << 20)
+    args.update(kw)
+    return ops.cs_prefill_paged_attn_ws_raw(**args)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=-1), ops.CS_ERR_INVALID_ARG),
+    (dict(head_dim=96), ops.CS_ERR_UNSUPPORTED),
+    (dict(scale=0.0), ops.CS_ERR_UNSUPPORTED),
+    (dict(q=None), ops.CS_ERR_INVALID_ARG),
+    (dict(workspace_bytes=-1), ops.CS_ERR_INVALID_ARG),
+])
+def test_prefill_ws_rejects_bad_arguments_before_any_gpu_call(kw, status):
+    assert attn_ws(**kw) == status
+
+
+def test_prefill_ws_empty_batch_is_a_noop():
+    assert attn_ws(batch=0, q=None, workspace=None, workspace_bytes=0) == ops.CS_OK
