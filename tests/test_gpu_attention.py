@@ -221,7 +221,17 @@ def test_llama70b_prefetch_pipeline_driven_by_the_control_plane(P):
     print(f"[case] llama70b_prefetch scout-driven pipeline total_q={wl.total_q}", flush=True)
     dw = pipeline.DeviceWorkload(wl)
     agents = sorted({inv.agent for inv in wl.invocations})
-    pipe = pipeline.AgentPipeline(dw, policy=pipeline.ScoutPolicy(wl, agents))
+    policy = pipeline.ScoutPolicy(wl, agents)
+    # record every turn's decision of the C++ control plane
+    decisions = []
+    on_turn = policy.on_turn
+
+    def recording_on_turn(a):
+        t = on_turn(a)
+        decisions.append((a, t))
+        return t
+    policy.on_turn = recording_on_turn
+    pipe = pipeline.AgentPipeline(dw, policy=policy)
     pipe.stage_first()
     for p in range(3):
         dw.out.fill_(float("nan"))
@@ -230,6 +240,17 @@ def test_llama70b_prefetch_pipeline_driven_by_the_control_plane(P):
         print(f"    pass {p}: hits={pipe.hits} misses={pipe.misses}", flush=True)
     n = len(pipe.agents)
     assert pipe.misses == n - 1 and pipe.hits == 2 * n + 1
+    # the same turns replayed through the oracle control plane (Eq. (3)-(11),
+    # the runtime procedure) give the same prefetch target at every turn
+    import oracle.control_plane as ocp
+    ref = ocp.ControlPlane(len(agents), wl.num_blocks)
+    for now, (a, t) in enumerate(decisions):
+        blocks, tokens = policy.touches[a]
+        for b, tk in zip(blocks.tolist(), tokens.tolist()):
+            ref.observe_touch(b, policy.ids[a], tk, now)
+        want = ref.between_step()
+        assert (None if want is None else policy.by_id.get(want)) == t, (now, a, t, want)
+    print(f"    {len(decisions)} decisions equal to the oracle control plane's", flush=True)
     kp, vp = oracle.kv_prefetch(wl.host_k, wl.host_v, wl.prefetch_dst, wl.k_pool, wl.v_pool)
     samples = sample_rows(wl, 300, seed=4)
     mx, mean = compare_rows(wl, dw.out_bits(), samples, kp, vp)
