@@ -672,6 +672,8 @@ def main():
     ap.add_argument("--workload", default="llama70b_prefetch",
                     choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-clock", action="store_true",
+                    help="skip the amd-smi clock / power sampling after the timed region")
     ap.add_argument("--no-workspace", action="store_true",
                     help="run the plain cs_prefill_paged_attn; by default the attention runs "
                          "cs_prefill_paged_attn_ws, which splits launches too small to fill the "
@@ -890,7 +892,7 @@ def main():
     # the clock the chip holds under this load, sampled over a few seconds of
     # the same steps after everything above (the timed region is too short
     # for amd-smi), and the fraction of the peak at that clock
-    clk = sample_clock_power(warm)
+    clk = {"skipped": True} if args.no_clock else sample_clock_power(warm)
     result["clock"] = clk
     if clk.get("sclk_mhz_median"):
         peak_at = PEAK_BF16_TFLOPS * clk["sclk_mhz_median"] / PEAK_SCLK_MHZ
