@@ -41,6 +41,9 @@ DESCRIPTIONS = {
                          "16384-block pool; 64 of each agent's 256 anchor blocks are "
                          "prefetched from pinned host memory on a side stream while the "
                          "previous agent's attention runs",
+    "tiny": "1 request, 8 query / 2 KV heads, head_dim 64, cached prefix 256 + suffix 64 "
+            "tokens, prefix blocks at a seeded permutation of a 64-block pool (a correctness "
+            "shape: one launch of 4 work-groups)",
     "llama8b": "1 request, 32 query / 8 KV heads, head_dim 128, cached prefix 2048 + suffix "
                "1024 tokens, 16384-block pool",
     "agent_batch": "32 invocations over 4 agents, anchors U[1536,3072], suffixes U[256,2048], "
@@ -98,7 +101,7 @@ def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim,
             return f"prefill_paged_attn_ppd_kernel<128, {'true' if tail else 'false'}>"
         return f"prefill_paged_attn_pp_kernel<{head_dim}, {'true' if tail else 'false'}>"
     if head_dim == 128:
-        return "prefill_paged_attn_ppd_split_kernel<128>"
+        return "prefill_paged_attn_ppd_split_kernel<128, false>"
     return f"prefill_paged_attn_kernel<{head_dim}, false, true>"
 
 
