@@ -200,6 +200,25 @@ def _time_launches(fn, steps, warmup, stream):
     return wall, sum(ms) / steps, ms
 
 
+def hbm_reference(dev, stream, nbytes=2 << 30):
+    """What plain library kernels reach on this GPU's HBM, measured beside an
+    HBM-bound component: torch's device-to-device copy (reads and writes
+    nbytes each) and its float32 sum (reads nbytes).  A practical ceiling for
+    comparison; the roofline fraction stays against the published peak."""
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).uniform_()
+    dst = torch.empty_like(src)
+    acc = torch.empty((), dtype=torch.float32, device=dev)
+    _, ms_copy, _ = _time_launches(lambda: dst.copy_(src), 10, 2, stream)
+    _, ms_sum, _ = _time_launches(lambda: torch.sum(src, 0, out=acc), 10, 2, stream)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes": nbytes,
+            "copy_gbs": round(2 * nbytes / (ms_copy * 1e-3) / 1e9, 1),
+            "read_sum_gbs": round(nbytes / (ms_sum * 1e-3) / 1e9, 1),
+            "note": "torch copy_ (read + write) and sum (read) of a 2 GiB float32 tensor"}
+
+
 def percentiles_us(ms_list):
     """Median, p10 and p90 of launch durations given in milliseconds, in us."""
     import numpy as np
@@ -468,6 +487,8 @@ def bench_copy(args, dev):
                  "logical_rate_gbs": round(logical / (avg_ms * 1e-3) / 1e9, 2),
                  "note": "achieved counts each distinct K/V block once (plus q and out); "
                          "logical counts the K/V of every key of every sequence"}
+    if args.component in ("decode", "cascade_decode", "kv_write"):
+        extra["hbm_reference"] = hbm_reference(dev, stream)
     return {"metric": f"{args.component} GB/s, 1 MI355X", "value": round(gbs, 2), "unit": "GB/s",
             "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
             "ms_per_step": round(wall / args.steps * 1e3, 4), "higher_is_better": True,
