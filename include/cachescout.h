@@ -32,15 +32,17 @@
  *   - Every pointer is caller-owned.  The GPU calls allocate no device or
  *     host memory and keep no state beyond a per-process cache of device
  *     properties (the compute-unit count of each device, read once, which
- *     sizes the attention launch); they are reentrant and may run
- *     concurrently on different streams.
+ *     sizes the attention launch) and the fixed device array of
+ *     cs_cascade_decode_attn_noalloc; they are reentrant and may run
+ *     concurrently on different streams (except that allocation-free call,
+ *     whose calls on one GPU share that array).
  *   - The attention launch orders its work-groups for MI355X's 8 XCDs
  *     (consecutive work-groups dealt round-robin to the XCDs, one L2 each);
  *     on a part with another XCD count the result is the same, only the L2
  *     reuse differs.  The control plane (cs_scout_*, at the end of this file) is
  *     host-only and owns the host memory behind its handle.
- *   - Every call enqueues its kernel on `stream` (NULL = the legacy default
- *     stream of the current device) and return without synchronizing.  Device
+ *   - Every call enqueues its kernels on `stream` (NULL = the legacy default
+ *     stream of the current device) and returns without synchronizing.  Device
  *     metadata is read by the kernels, never by the host, so the calls can be
  *     captured in a HIP graph (unless CS_DEBUG_CHECK=1, see below).
  *   - The device is the caller's current HIP device; every device pointer
