@@ -46,6 +46,9 @@
 // matrix work overlaps the other's vector work between two barriers.  The
 // K/V tiles serve 8 waves instead of 4 (waves 0-3 stage K, 4-7 stage V), and
 // each row's arithmetic is the same as in the four-wave kernel, bit for bit.
+// The ppd kernels are this design with K and V loaded straight into LDS
+// (head_dim 128, and head_dim 64 launches without a split tail; at head_dim
+// 64 two work-groups share a CU).
 //
 // Split launches (less than a round of ping-pong tiles): a four-wave
 // tile alone on a CU would leave one wave per SIMD, with nothing to hide its
@@ -140,18 +143,39 @@ struct Lds {
   uint16_t v[2][kBN * vStride];               // V of steps j
 };
 
-// Direct-to-LDS staging (the D = 128 kernels).  buffer_load_dwordx4 with the
+// Direct-to-LDS staging (the ppd kernels).  buffer_load_dwordx4 with the
 // LDS flag writes lane i's 16 bytes at the instruction's LDS address + 16 i,
-// so one load moves four 256-byte rows of a (block, head) tile (1 KB).  A
-// buffer holds one 64-key step as 16 four-row groups 4 D + 8 elements apart
-// (16 bytes of padding); inside a group, the 16-byte chunk s of row d holds
-// the row's chunk s ^ 4d.  The K operand reads (ds_read_b128: 8 rows, one
-// chunk per 8 lanes) and the transposing V reads (4 rows, 4 chunks per 32
-// lanes) are then free of bank conflicts at 64 banks, and every per-lane
-// address is one register plus a constant.  Buffer loads rather than
-// global_load_lds: the compiler's wait insertion counts a global load into
-// LDS as a flat access and then makes every LDS read wait for all loads in
-// flight; with buffer loads it keeps exact counts.
+// so one load moves 1 KB of a (block, head) tile: four 256-byte rows at
+// D = 128, eight 128-byte rows at D = 64 (a "group").  Which 16-byte chunk
+// each lane fetches is free, so the layout inside a group is any
+// permutation of its chunks.  A buffer holds one 64-key step as 16 (D = 128)
+// or 8 (D = 64) groups.
+//   D = 128: groups 4 D + 8 elements apart (16 bytes of padding); chunk s of
+//            row d holds the row's chunk s ^ 4d.
+//   D = 64:  groups 8 D + 16 elements apart (32 bytes); chunk s of row d
+//            holds the row's chunk s ^ y(d), y(d) = 4 ((d / 2) % 2) + d / 4.
+// The K operand reads (ds_read_b128: 16 lanes, one chunk of 16 rows, per
+// pass) and the transposing V reads (32 lanes, 64 bytes of 4 rows, per pass)
+// are then free of bank conflicts at 64 banks (checked element by element,
+// with the bank of every access, in the host layout test), and every
+// per-lane address is one register plus a constant.  Buffer loads rather
+// than global_load_lds: the compiler's wait insertion counts a global load
+// into LDS as a flat access and then makes every LDS read wait for all loads
+// in flight; with buffer loads it keeps exact counts.
+template <int D>
+struct DirectLayout;
+template <>
+struct DirectLayout<128> {
+  static constexpr int kRows = 4;                 // rows per 1 KB group
+  static constexpr int kGrp = 4 * 128 + 8;        // elements from group to group
+  static __device__ __forceinline__ int swz(int d) { return 4 * d; }
+};
+template <>
+struct DirectLayout<64> {
+  static constexpr int kRows = 8;
+  static constexpr int kGrp = 8 * 64 + 16;
+  static __device__ __forceinline__ int swz(int d) { return 4 * ((d >> 1) & 1) + (d >> 2); }
+};
 //
 // Word 3 of a raw buffer descriptor on gfx9-family parts: 32-bit data format
 // (DATA_FORMAT = 4), no swizzle, no index stride.
@@ -159,6 +183,7 @@ constexpr int kRawBufferWord3 = 0x00020000;
 // s_waitcnt immediates (gfx9 layout: vmcnt[3:0], expcnt[6:4], lgkmcnt[11:8],
 // vmcnt[5:4] at [15:14]; a field at its maximum does not wait)
 constexpr int kWaitVmcnt0 = 0x0F70;
+constexpr int kWaitVmcnt2 = 0x0F72;
 constexpr int kWaitVmcnt4 = 0x0F74;
 constexpr int kWaitLgkmcnt0 = 0xC07F;
 
@@ -1261,18 +1286,22 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   }
 }
 
-// The ping-pong kernel for D = 128 with direct-to-LDS staging: no round trip
-// through registers, so the 32 staging registers per lane go, and the loads
-// of a step have two iterations to land in a three-deep ring of K and V
-// buffers.  Same arithmetic in the same order as the ping-pong kernel, so
-// the results are bitwise equal.  kTail: as in the ping-pong kernel, the
-// work-groups from pp_grid on take half tiles of the launch's last round.
+// The ping-pong kernel with direct-to-LDS staging (D = 128 and 64): no
+// round trip through registers, so the staging registers per lane go, and
+// the loads of a step have two iterations to land in a three-deep ring of K
+// and V buffers.  Same arithmetic in the same order as the ping-pong kernel,
+// so the results are bitwise equal.  kTail (D = 128): as in the ping-pong
+// kernel, the work-groups from pp_grid on take half tiles of the launch's
+// last round.  At head_dim 64 the kernel holds at most 128 VGPRs (at least
+// four waves per SIMD) and 50,688 bytes of LDS, so two work-groups share a
+// CU.
 template <int D, bool kTail>
-__global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Params p) {
-  static_assert(D == 128, "direct-to-LDS staging is laid out for 256-byte rows");
+__global__ __launch_bounds__(kPPThreads, D == 64 ? 4 : 2) void prefill_paged_attn_ppd_kernel(Params p) {
+  static_assert(D == 128 || !kTail, "the split tail tile is laid out for 256-byte rows");
+  using DL = DirectLayout<D>;
   // K and V of three steps, each in its own array so that the compiler can
   // tell a read of one from a direct load in flight into another
-  constexpr int kBuf = 16 * (4 * D + 8);
+  constexpr int kBuf = (kBN / DL::kRows) * DL::kGrp;
   __shared__ __attribute__((aligned(16))) uint16_t k0[kBuf], k1[kBuf], k2[kBuf];
   __shared__ __attribute__((aligned(16))) uint16_t v0[kBuf], v1[kBuf], v2[kBuf];
   const int wg = blockIdx.x;
@@ -1335,8 +1364,13 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
 
   // ---- staging: waves 0-3 move K, waves 4-7 move V, straight from global
   // memory into LDS in the direct-to-LDS layout; wave w moves pool block
-  // 4*step + (w & 3)
-  constexpr int kGrp = 4 * D + 8;                      // elements per four-row group
+  // 4*step + (w & 3), kLoads groups of rows
+  constexpr int kGrp = DL::kGrp;                       // elements from group to group
+  constexpr int kLoads = kBlock / DL::kRows;           // 1 KB loads per block
+  // (a local constant: with the dependent DL::kRows written into the
+  // builtin's argument, this hipcc's host pass drops the kernel's launch
+  // stubs without a diagnostic)
+  constexpr int kGroupElems = DL::kRows * D;           // elements of one group's rows
   const int slot_u = __builtin_amdgcn_readfirstlane(wave & 3);
   const uint16_t* my_base = (group_b ? p.v_pool : p.k_pool) + (size_t)g * tile_elems;
   const __attribute__((address_space(4))) int32_t* bt_c =
@@ -1345,9 +1379,10 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
     const int lb = step * (kBN / kBlock) + slot_u;
     return (step < n_steps && lb < n_blk) ? bt_c[lb] : -1;          // -1: past the end
   };
-  // lane i of a load: row d = i / 16 of the group, stored chunk i % 16
-  const int dma_d = lane >> 4;
-  const int dma_off = dma_d * D + 8 * ((lane & 15) ^ (4 * dma_d));
+  // lane i of a load: row d = i / (D / 8) of the group, stored chunk
+  // i % (D / 8), which holds the row's chunk (i % (D / 8)) ^ swz(d)
+  const int dma_d = lane / (D / 8);
+  const int dma_off = dma_d * D + 8 * ((lane % (D / 8)) ^ DL::swz(dma_d));
   // a block past the end loads pool slot 0 (any valid slot): its K logits
   // are masked and its V rows zeroed
   auto dma = [&](uint16_t* buf, int id) __attribute__((always_inline)) {
@@ -1356,9 +1391,9 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
     const __amdgpu_buffer_rsrc_t rs =
         __builtin_amdgcn_make_buffer_rsrc((void*)blk, (short)0, (int)(tile_elems * sizeof(uint16_t)), kRawBufferWord3);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + (4 * slot_u + u) * kGrp),
-                                               16, 2 * dma_off, 2 * u * 4 * D, 0, 0);
+    for (int u = 0; u < kLoads; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + (kLoads * slot_u + u) * kGrp),
+                                               16, 2 * dma_off, 2 * u * kGroupElems, 0, 0);
   };
   // V rows past the end of the sequence (inside its last block, or whole
   // blocks past it) overwritten with zeros once their load has landed:
@@ -1366,32 +1401,52 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
   auto zero_tail = [&](uint16_t* buf, int key0) __attribute__((always_inline)) {
     if (key0 + kBlock > L) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (key0 + 4 * u + dma_d >= L)
-          *reinterpret_cast<uint4*>(&buf[(4 * slot_u + u) * kGrp + dma_d * D + 8 * (lane & 15)]) =
-              make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < kLoads; ++u) {
+        if (key0 + DL::kRows * u + dma_d >= L)
+          *reinterpret_cast<uint4*>(&buf[(kLoads * slot_u + u) * kGrp + 8 * lane]) = make_uint4(0, 0, 0, 0);
       }
     }
   };
-  // K operand: row mt*32 + qi (group 8 mt + qi/4, row qi%4), chunk 2 ks + half,
-  // stored at chunk half + 2 (ks%2) + 4 ((ks/2) ^ (qi%4))
-  int koff[4];
+  // K operand: row mt*32 + qi, chunk 2 ks + half.  D = 128: group 8 mt +
+  // qi/4, row qi%4, stored at chunk half + 2 (ks%2) + 4 ((ks/2) ^ (qi%4));
+  // D = 64: group 4 mt + qi/8, row qi%8, stored at chunk (2 ks + half) ^ y(qi%8)
+  constexpr int kKoff = D == 128 ? 4 : KS;
+  int koff[kKoff];
 #pragma unroll
-  for (int k2 = 0; k2 < 4; ++k2)
-    koff[k2] = (qi >> 2) * kGrp + (qi & 3) * D + 8 * half + 32 * (k2 ^ (qi & 3));
+  for (int k2 = 0; k2 < kKoff; ++k2) {
+    if constexpr (D == 128)
+      koff[k2] = (qi >> 2) * kGrp + (qi & 3) * D + 8 * half + 32 * (k2 ^ (qi & 3));
+    else
+      koff[k2] = (qi >> 3) * kGrp + (qi & 7) * D + 8 * ((2 * k2 + half) ^ DL::swz(qi & 7));
+  }
+  auto k_addr = [&](const uint16_t* kbuf, int ks, int mt) __attribute__((always_inline)) -> const uint16_t* {
+    if constexpr (D == 128) return &kbuf[mt * 8 * kGrp + 16 * (ks & 1) + koff[ks >> 1]];
+    else return &kbuf[mt * 4 * kGrp + koff[ks]];
+  };
   // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
   // transposing reads; lane 16e + i addresses key 4*(e/2) + i/4 and dims
   // 16*(e%2) + 4*(i%4) .. +3, an 8-byte half of chunk 4 dt + jc with
   // jc = 2 (e%2) + (i%4)/2, stored at chunk 4 (dt ^ d) + jc of its row d
+  // (D = 64: key 16 ks2 + tr_row of the lo read is row tr_row of group 2 ks2,
+  // the hi read's the same row of group 2 ks2 + 1; the lane's 8 bytes are
+  // half (lane % 2) of chunk 4 dt + 2 ((lane / 16) % 2) + (lane % 4) / 2)
   const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
-  const int tr_d = tr_row & 3;
-  const int tr_base = (tr_row >> 2) * kGrp + tr_d * D + 8 * (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) + 4 * (lane & 1);
   int voff[DT];
+  if constexpr (D == 128) {
+    const int tr_d = tr_row & 3;
+    const int tr_base = (tr_row >> 2) * kGrp + tr_d * D + 8 * (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) + 4 * (lane & 1);
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) voff[dt] = tr_base + 32 * (dt ^ tr_d);
+    for (int dt = 0; dt < DT; ++dt) voff[dt] = tr_base + 32 * (dt ^ tr_d);
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      voff[dt] = tr_row * D + 8 * ((4 * dt + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) ^ DL::swz(tr_row)) + 4 * (lane & 1);
+  }
+  constexpr int kSliceGroups = 16 / DL::kRows;        // groups per 16-key slice
   auto v_frag = [&](const uint16_t* vbuf, int ks2, int dt) __attribute__((always_inline)) -> bf16x8 {
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + 4 * ks2 * kGrp + voff[dt]));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + 4 * ks2 * kGrp + 2 * kGrp + voff[dt]));
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + kSliceGroups * ks2 * kGrp + voff[dt]));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(vbuf + kSliceGroups * ks2 * kGrp + (kSliceGroups / 2) * kGrp + voff[dt]));
     const i16x4 lohi[2] = {lo, hi};
     return __builtin_bit_cast(bf16x8, lohi);
   };
@@ -1419,7 +1474,7 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
         for (int ks = 0; ks < KS; ++ks) {
   #pragma unroll
           for (int mt = 0; mt < 2; ++mt) {
-            const uint4 a = *reinterpret_cast<const uint4*>(&kbuf[mt * 8 * kGrp + 16 * (ks & 1) + koff[ks >> 1]]);
+            const uint4 a = *reinterpret_cast<const uint4*>(k_addr(kbuf, ks, mt));
             s_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], s_acc[mt], 0, 0, 0);
           }
         }
@@ -1508,9 +1563,9 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
     // K waves load K_0 and K_1, V waves V_0.  Iteration j reads K_j and
     // V_{j-1} and issues K_{j+2} (K waves) or V_{j+1} (V waves) into the
     // buffer of the step three back, read in iteration j-1; every wave issues
-    // exactly four loads per iteration (a step past the last loads slot 0 into
-    // a buffer nothing reads again), so waiting until at most four are in
-    // flight before the barrier completes the loads of the data read next.
+    // exactly kLoads loads per iteration (a step past the last loads slot 0
+    // into a buffer nothing reads again), so waiting until at most kLoads are
+    // in flight before the barrier completes the loads of the data read next.
     int id_next;     // block of the step the next iteration loads, read ahead
     if (!kB) {
       dma(k0, block_id(0));
@@ -1523,9 +1578,9 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_kernel(Para
 
     auto iteration = [&](const int j, uint16_t* kcur, uint16_t* knext2, uint16_t* vprev,
                          uint16_t* vnext) __attribute__((always_inline)) {
-      // loads issued two iterations back have landed (vmcnt <= 4); the V
-      // block read in this iteration gets its tail zeroed; then the barrier
-      __builtin_amdgcn_s_waitcnt(kWaitVmcnt4);
+      // loads issued two iterations back have landed (vmcnt <= kLoads); the
+      // V block read in this iteration gets its tail zeroed; then the barrier
+      __builtin_amdgcn_s_waitcnt(D == 128 ? kWaitVmcnt4 : kWaitVmcnt2);
       if (kB && j >= 1) zero_tail(vprev, (j - 1) * kBN + slot_u * kBlock);
       __builtin_amdgcn_s_waitcnt(kWaitLgkmcnt0);
       asm volatile("s_barrier" ::: "memory");
@@ -1730,7 +1785,7 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
     } else if (tail) {
       hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<64, true>), grid, dim3(kPPThreads), 0, stream, p);
     } else {
-      hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<64, false>), grid, dim3(kPPThreads), 0, stream, p);
+      hipLaunchKernelGGL((prefill_paged_attn_ppd_kernel<64, false>), grid, dim3(kPPThreads), 0, stream, p);
     }
   } else if (a.head_dim == 128) {
     // fewer than one ping-pong work-group per CU: 128-row tiles, each run

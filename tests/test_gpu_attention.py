@@ -123,54 +123,74 @@ def test_ping_pong_launch_with_split_tail(P, name):
     check_full(P, wl)
 
 
-@pytest.mark.parametrize("shape", ["split", "ping_pong", "ping_pong_tail"])
+PP_INVS = {"split": [Invocation(0, 37), Invocation(1, 90), Invocation(0, 5)],
+           "ping_pong": [Invocation(i % 2, 1000 + 13 * i) for i in range(2)],
+           "ping_pong_d64": [Invocation(i % 2, 1000 + 13 * i) for i in range(2)],
+           "ping_pong_tail": [Invocation(i % 2, 450 + 7 * i) for i in range(5)]}
+
+
+def pp_head_dim(shape):
+    return 64 if shape.endswith("_d64") else 128
+
+
+@pytest.mark.parametrize("shape", ["split", "ping_pong", "ping_pong_d64", "ping_pong_tail"])
 def test_slot_zero_full_of_nan(P, shape):
     """Blocks past a sequence's end are loaded from pool slot 0 and then
     masked (K) or zeroed (V): with slot 0 all NaN the output stays exact."""
     ops, _ = P
-    invs = {"split": [Invocation(0, 37), Invocation(1, 90), Invocation(0, 5)],
-            "ping_pong": [Invocation(i % 2, 1000 + 13 * i) for i in range(2)],
-            "ping_pong_tail": [Invocation(i % 2, 450 + 7 * i) for i in range(5)]}[shape]
-    wl = build_workload("nan_slot0", 6, [61, 200], invs, num_q_heads=32, num_kv_heads=8,
-                        head_dim=128, num_blocks=512)
+    wl = build_workload("nan_slot0", 6, [61, 200], PP_INVS[shape], num_q_heads=32, num_kv_heads=8,
+                        head_dim=pp_head_dim(shape), num_blocks=512)
     u = poison_slot_zero(wl)
     print(f"[case] slot 0 all NaN, {shape}: its blocks moved to slot {u}", flush=True)
     check_full(P, wl)
 
 
-@pytest.mark.parametrize("shape", ["ping_pong", "ping_pong_tail"])
+@pytest.mark.parametrize("shape", ["ping_pong", "ping_pong_d64", "ping_pong_tail"])
 def test_peaky_logits_on_the_ping_pong_paths(P, shape):
     """Queries scaled up 8x (logits in the tens of log2 units): the large
     launches' kernels keep the scale in fp32 and stay within tolerance too."""
     ops, _ = P
-    invs = {"ping_pong": [Invocation(i % 2, 1000 + 13 * i) for i in range(2)],
-            "ping_pong_tail": [Invocation(i % 2, 450 + 7 * i) for i in range(5)]}[shape]
-    wl = build_workload("peaky_pp", 8, [61, 200], invs, num_q_heads=32, num_kv_heads=8,
-                        head_dim=128, num_blocks=512, q_gain=8.0)
+    wl = build_workload("peaky_pp", 8, [61, 200], PP_INVS[shape], num_q_heads=32, num_kv_heads=8,
+                        head_dim=pp_head_dim(shape), num_blocks=512, q_gain=8.0)
     kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, 32, 8)
     assert kernel == ops.ATTN_PING_PONG and (tail > 0) == (shape == "ping_pong_tail")
     print(f"[case] peaky logits, {shape}: grid={grid} tail={tail}", flush=True)
     check_full(P, wl)
 
 
-@pytest.mark.parametrize("shape", ["split", "ping_pong", "ping_pong_tail"])
+@pytest.mark.parametrize("shape", ["split", "ping_pong", "ping_pong_d64", "ping_pong_tail"])
 def test_nan_and_inf_past_the_end_do_not_leak(P, shape):
     """Pool positions past a sequence's end inside its last block may hold
     anything (a recycled slot): NaN and Inf there must not reach the output,
     on every kernel path."""
     ops, _ = P
-    invs = {"split": [Invocation(0, 37), Invocation(1, 90), Invocation(0, 5)],
-            "ping_pong": [Invocation(i % 2, 1000 + 13 * i) for i in range(2)],
-            "ping_pong_tail": [Invocation(i % 2, 450 + 7 * i) for i in range(5)]}[shape]
-    wl = build_workload("nan_tail", 5, [61, 200], invs, num_q_heads=32, num_kv_heads=8,
-                        head_dim=128, num_blocks=512)
+    wl = build_workload("nan_tail", 5, [61, 200], PP_INVS[shape], num_q_heads=32, num_kv_heads=8,
+                        head_dim=pp_head_dim(shape), num_blocks=512)
     kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, 32, 8)
     assert (kernel, tail > 0) == {"split": (ops.ATTN_SPLIT, False),
                                   "ping_pong": (ops.ATTN_PING_PONG, False),
+                                  "ping_pong_d64": (ops.ATTN_PING_PONG, False),
                                   "ping_pong_tail": (ops.ATTN_PING_PONG, True)}[shape]
     n = poison_tails(wl)
     print(f"[case] nan tails, {shape}: {n} poisoned positions, grid={grid}", flush=True)
     assert n > 0
+    check_full(P, wl)
+
+
+@pytest.mark.parametrize("prefix,suffix,n_inv", [(2048, 512, 16), (0, 512, 16), (37, 300, 32)])
+def test_head_dim_64_ping_pong_full(P, prefix, suffix, n_inv):
+    """head_dim 64 launches of whole rounds (the direct-to-LDS ping-pong kernel
+    with its eight-row LDS groups), every output element against the oracle:
+    prefix hits, misses with the causal triangle only, and a prefix that is
+    not a multiple of the block size with a ragged last token tile."""
+    ops, _ = P
+    invs = [Invocation(0, suffix - (i % 3)) for i in range(n_inv)]
+    wl = build_workload("pp_d64", 17, [prefix], invs, num_q_heads=32, num_kv_heads=8,
+                        head_dim=64, num_blocks=prefix // 16 + n_inv * (suffix // 16 + 2) + 64)
+    kernel, grid, tail = ops.prefill_launch_shape(wl.batch, wl.max_q_len, 32, 8)
+    print(f"[case] head_dim 64 ping-pong P={prefix} S={suffix} x{n_inv}: grid={grid} tail={tail}",
+          flush=True)
+    assert kernel == ops.ATTN_PING_PONG and tail == 0
     check_full(P, wl)
 
 
