@@ -56,6 +56,8 @@ constexpr int kDecodeWaves = 12;
 constexpr int kCascadeWaves = 4;
 constexpr int kThreads = 256;        // the merge kernel
 constexpr int kMaxGroup = 16;
+// plain decode batches up to this size run longest sequence first
+constexpr int kLptMaxBatch = 1024;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct DecParams {
@@ -132,7 +134,33 @@ __global__ __launch_bounds__(64 * (kCascade ? kCascadeWaves : kDecodeWaves)) voi
     r = (blockIdx.x / p.num_kv_heads) % p.batch;
     seg = blockIdx.x / p.num_kv_heads / p.batch;
   } else {
+    // Longest sequence first: the work-groups of one wave of dispatch take
+    // the sequences of ranks w / num_kv_heads in decreasing length (ties by
+    // index), so the last of the launch's rounds holds the shortest ones
+    // and the CUs run out of work together.  Every work-group ranks the
+    // lengths itself (each thread a few candidates against all of them, in
+    // LDS): the order is a permutation whatever the lengths hold, so every
+    // (sequence, head) is still computed exactly once, and each output is
+    // the same as in any other order.
     r = blockIdx.x / p.num_kv_heads;
+    if (p.batch <= kLptMaxBatch) {
+      __shared__ int lens[kLptMaxBatch];
+      __shared__ int pick;
+      for (int s = threadIdx.x; s < p.batch; s += kWGThreads) lens[s] = p.seq_lens[s];
+      if (threadIdx.x == 0) pick = r;
+      __syncthreads();
+      for (int s = threadIdx.x; s < p.batch; s += kWGThreads) {
+        const int ls = lens[s];
+        int rank = 0;
+        for (int t = 0; t < p.batch; ++t) {
+          const int lt = lens[t];
+          rank += (lt > ls) || (lt == ls && t < s);
+        }
+        if (rank == r) pick = s;
+      }
+      __syncthreads();
+      r = pick;
+    }
   }
   const int L = p.seq_lens[r];
   int start = 0;       // keys start .. end - 1 are this work-group's
@@ -397,6 +425,7 @@ hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream) {
   p.num_kv_heads = a.num_kv_heads;
   p.group = a.num_q_heads / a.num_kv_heads;
   p.scale_log2 = a.scale * kLog2e;
+  p.batch = a.batch;
   const dim3 grid((unsigned)((long long)a.batch * a.num_kv_heads)), block(64 * kDecodeWaves);
   if (a.head_dim == 128) {
     hipLaunchKernelGGL((paged_decode_attn_kernel<128, false>), grid, block, 0, stream, p);
