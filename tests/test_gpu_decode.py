@@ -286,3 +286,49 @@ def test_decode_private_recipe_scaled_down():
                         head_dim=128, occupancy=0.9)
     print(f"[case] decode_private scaled down: kv_lens={wl.kv_lens.tolist()}", flush=True)
     check(run_decode(wl), oracle_last_rows(wl), "decode vs oracle")
+
+
+def decode_bits(q, k_pool, v_pool, bt, seq_lens, scale):
+    from paper_2608_14624_amd import ops
+    qd = dev_bf16(q)
+    out = torch.empty_like(qd)
+    ops.cs_paged_decode_attn(qd, k_pool, v_pool, torch.from_numpy(np.ascontiguousarray(bt)).cuda(),
+                             torch.from_numpy(np.ascontiguousarray(seq_lens)).cuda(), out,
+                             max_seq_len=int(seq_lens.max()), scale=scale)
+    torch.cuda.synchronize()
+    return out.view(torch.int16).cpu().numpy()
+
+
+def test_decode_is_independent_of_batch_order():
+    """The kernel runs the sequences longest first (every work-group ranks
+    the lengths itself, ties by index): reordering the batch, with many
+    equal lengths, permutes the output rows and changes no bit of them."""
+    invs = [Invocation(i % 5, 1 + (i % 4) * 17) for i in range(40)]   # ten of each length class
+    wl = build_workload("order", 3, [30, 61, 16, 100, 5], invs, num_q_heads=8, num_kv_heads=2,
+                        head_dim=128, num_blocks=1024)
+    q, seq_lens = decode_view(wl)
+    assert len(np.unique(seq_lens)) < len(seq_lens)
+    kp, vp = dev_bf16(wl.k_pool), dev_bf16(wl.v_pool)
+    base = decode_bits(q, kp, vp, wl.block_tables, seq_lens, wl.scale)
+    for seed in (1, 2):
+        perm = np.random.default_rng(seed).permutation(wl.batch)
+        got = decode_bits(q[perm], kp, vp, wl.block_tables[perm], seq_lens[perm], wl.scale)
+        assert np.array_equal(got, base[perm])
+    ref = oracle_last_rows(wl)
+    out = oracle.bf16_bits_to_f64(base.view(np.uint16))
+    err = np.abs(out - ref)
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
+
+
+def test_decode_batch_past_the_ranking_limit():
+    """Batches above 1024 sequences run in dispatch order: 1100 sequences
+    give bit for bit what their two halves give (each ranked)."""
+    invs = [Invocation(i % 3, 1 + (7 * i) % 40) for i in range(1100)]
+    wl = build_workload("big_batch", 4, [20, 33, 70], invs, num_q_heads=4, num_kv_heads=4,
+                        head_dim=64, num_blocks=8192)
+    q, seq_lens = decode_view(wl)
+    kp, vp = dev_bf16(wl.k_pool), dev_bf16(wl.v_pool)
+    whole = decode_bits(q, kp, vp, wl.block_tables, seq_lens, wl.scale)
+    a = decode_bits(q[:600], kp, vp, wl.block_tables[:600], seq_lens[:600], wl.scale)
+    b = decode_bits(q[600:], kp, vp, wl.block_tables[600:], seq_lens[600:], wl.scale)
+    assert np.array_equal(whole, np.concatenate([a, b]))
