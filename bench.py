@@ -97,14 +97,8 @@ def attention_kernel_name(batch, max_q_len, num_q_heads, num_kv_heads, head_dim,
                 f"prefill_split_merge_kernel<{head_dim}>")
     kernel, _, tail = ops.prefill_launch_shape(batch, max_q_len, num_q_heads, num_kv_heads)
     if kernel == ops.ATTN_PING_PONG:
-        if head_dim == 128:
-            return f"prefill_paged_attn_ppd_kernel<128, {'true' if tail else 'false'}>"
-        if not tail:
-            return "prefill_paged_attn_ppd_kernel<64, false>"
-        return "prefill_paged_attn_pp_kernel<64, true>"
-    if head_dim == 128:
-        return "prefill_paged_attn_ppd_split_kernel<128, false>"
-    return f"prefill_paged_attn_kernel<{head_dim}, false, true>"
+        return f"prefill_paged_attn_ppd_kernel<{head_dim}, {'true' if tail else 'false'}>"
+    return f"prefill_paged_attn_ppd_split_kernel<{head_dim}, false>"
 
 
 def key_parts(sb, wl, workspace):

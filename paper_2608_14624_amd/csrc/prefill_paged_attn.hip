@@ -977,7 +977,10 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
                                                uint16_t* v2, uint16_t* v3) {
   constexpr int KS = D / 16;     // MFMA k-steps over the head dim
   constexpr int DT = D / 32;     // 32-wide output tiles over the head dim
-  constexpr int kGrp = 4 * D + 8;
+  using DL = DirectLayout<D>;
+  constexpr int kGrp = DL::kGrp;
+  constexpr int kLoads = kBlock / DL::kRows;           // 1 KB loads per block
+  constexpr int kGroupElems = DL::kRows * D;           // (a local constant, as in the ppd kernel)
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = (tid >> 6) & 3;                 // row owner within the half
@@ -1061,40 +1064,57 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
     const int lb = (j0 + step) * (kBN / kBlock) + slot_u;
     return (step < n_steps && lb < n_blk) ? bt_c[lb] : -1;          // -1: past the end
   };
-  const int dma_d = lane >> 4;
-  const int dma_off = dma_d * D + 8 * ((lane & 15) ^ (4 * dma_d));
+  // staging and operand addressing as in the ppd kernel (DirectLayout<D>)
+  const int dma_d = lane / (D / 8);
+  const int dma_off = dma_d * D + 8 * ((lane % (D / 8)) ^ DL::swz(dma_d));
   auto dma = [&](uint16_t* buf, const uint16_t* base, int id) __attribute__((always_inline)) {
     const uint16_t* blk = base + (size_t)(id >= 0 ? id : 0) * slot_elems;
     const __amdgpu_buffer_rsrc_t rs =
         __builtin_amdgcn_make_buffer_rsrc((void*)blk, (short)0, (int)(tile_elems * sizeof(uint16_t)), kRawBufferWord3);
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + (4 * slot_u + u) * kGrp),
-                                               16, 2 * dma_off, 2 * u * 4 * D, 0, 0);
+    for (int u = 0; u < kLoads; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + (kLoads * slot_u + u) * kGrp),
+                                               16, 2 * dma_off, 2 * u * kGroupElems, 0, 0);
   };
   auto zero_tail = [&](uint16_t* buf, int key0) __attribute__((always_inline)) {
     if (key0 + kBlock > L) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (key0 + 4 * u + dma_d >= L)
-          *reinterpret_cast<uint4*>(&buf[(4 * slot_u + u) * kGrp + dma_d * D + 8 * (lane & 15)]) =
-              make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < kLoads; ++u) {
+        if (key0 + DL::kRows * u + dma_d >= L)
+          *reinterpret_cast<uint4*>(&buf[(kLoads * slot_u + u) * kGrp + 8 * lane]) = make_uint4(0, 0, 0, 0);
       }
     }
   };
-  int koff[4];
+  constexpr int kKoff = D == 128 ? 4 : KS;
+  int koff[kKoff];
 #pragma unroll
-  for (int k2i = 0; k2i < 4; ++k2i)
-    koff[k2i] = (qi >> 2) * kGrp + (qi & 3) * D + 8 * half + 32 * (k2i ^ (qi & 3));
+  for (int k2i = 0; k2i < kKoff; ++k2i) {
+    if constexpr (D == 128)
+      koff[k2i] = (qi >> 2) * kGrp + (qi & 3) * D + 8 * half + 32 * (k2i ^ (qi & 3));
+    else
+      koff[k2i] = (qi >> 3) * kGrp + (qi & 7) * D + 8 * ((2 * k2i + half) ^ DL::swz(qi & 7));
+  }
+  auto k_addr = [&](const uint16_t* kbuf, int ks, int mt) __attribute__((always_inline)) -> const uint16_t* {
+    if constexpr (D == 128) return &kbuf[mt * 8 * kGrp + 16 * (ks & 1) + koff[ks >> 1]];
+    else return &kbuf[mt * 4 * kGrp + koff[ks]];
+  };
   const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
-  const int tr_d = tr_row & 3;
-  const int tr_base = (tr_row >> 2) * kGrp + tr_d * D + 8 * (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) + 4 * (lane & 1);
   int voff[DT];
+  if constexpr (D == 128) {
+    const int tr_d = tr_row & 3;
+    const int tr_base = (tr_row >> 2) * kGrp + tr_d * D + 8 * (2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) + 4 * (lane & 1);
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) voff[dt] = tr_base + 32 * (dt ^ tr_d);
+    for (int dt = 0; dt < DT; ++dt) voff[dt] = tr_base + 32 * (dt ^ tr_d);
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      voff[dt] = tr_row * D + 8 * ((4 * dt + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1)) ^ DL::swz(tr_row)) + 4 * (lane & 1);
+  }
+  constexpr int kSliceGroups = 16 / DL::kRows;        // groups per 16-key slice
   auto v_frag = [&](const uint16_t* vbuf, int ks2, int dt) __attribute__((always_inline)) -> bf16x8 {
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + 4 * ks2 * kGrp + voff[dt]));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + 4 * ks2 * kGrp + 2 * kGrp + voff[dt]));
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vbuf + kSliceGroups * ks2 * kGrp + voff[dt]));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4*)(vbuf + kSliceGroups * ks2 * kGrp + (kSliceGroups / 2) * kGrp + voff[dt]));
     const i16x4 lohi[2] = {lo, hi};
     return __builtin_bit_cast(bf16x8, lohi);
   };
@@ -1117,7 +1137,7 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
     for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
-        const uint4 a = *reinterpret_cast<const uint4*>(&kbuf[mt * 8 * kGrp + 16 * (ks & 1) + koff[ks >> 1]]);
+        const uint4 a = *reinterpret_cast<const uint4*>(k_addr(kbuf, ks, mt));
         s_cur[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], s_cur[mt], 0, 0, 0);
       }
     }
@@ -1230,8 +1250,11 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
   float l_tot = pair_sum(l_run);
   // ---- merge: wave w of the second half hands (O, m, l) of its rows to
-  // wave w of the first through one 16640-byte buffer: value e of lane l at
-  // word 64 e + l, m and l of query qi at words 4096 + qi and 4128 + qi
+  // wave w of the first through one staging buffer (16640 bytes at head_dim
+  // 128, 8448 at 64: exactly what it takes): value e of lane l at word
+  // 64 e + l, m and l of query qi at words kMl + qi and kMl + 32 + qi
+  constexpr int kMl = DT * 16 * 64;
+  static_assert(kMl + 64 <= (kBN / DL::kRows) * DL::kGrp / 2, "merge exchange exceeds a staging buffer");
   float* x = reinterpret_cast<float*>(wave == 0 ? k0 : wave == 1 ? k1 : wave == 2 ? v0 : v1);
   __syncthreads();
   if (split_half == 1) {
@@ -1239,12 +1262,12 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int rr = 0; rr < 16; ++rr) x[(dt * 16 + rr) * 64 + lane] = oacc[dt][rr];
-    x[64 * 64 + 32 * half + qi] = half ? l_tot : m_run;
+    x[kMl + 32 * half + qi] = half ? l_tot : m_run;
   }
   __syncthreads();
   if (split_half == 1) return;
-  const float m1 = x[64 * 64 + qi];
-  const float l1 = x[64 * 64 + 32 + qi];
+  const float m1 = x[kMl + qi];
+  const float l1 = x[kMl + 32 + qi];
   const float mx = fmaxf(m_run, m1);
   const float w0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run - mx) * c);
   const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m1 - mx) * c);
@@ -1290,14 +1313,13 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
 // round trip through registers, so the staging registers per lane go, and
 // the loads of a step have two iterations to land in a three-deep ring of K
 // and V buffers.  Same arithmetic in the same order as the ping-pong kernel,
-// so the results are bitwise equal.  kTail (D = 128): as in the ping-pong
-// kernel, the work-groups from pp_grid on take half tiles of the launch's
-// last round.  At head_dim 64 the kernel holds at most 128 VGPRs (at least
-// four waves per SIMD) and 50,688 bytes of LDS, so two work-groups share a
-// CU.
+// so the results are bitwise equal.  kTail: as in the ping-pong kernel, the
+// work-groups from pp_grid on take half tiles of the launch's last round.
+// At head_dim 64 the kernel holds at most 128 VGPRs (at least four waves per
+// SIMD) and 50,688 bytes of LDS (67,584 with the tail's two more buffers),
+// so two work-groups share a CU.
 template <int D, bool kTail>
 __global__ __launch_bounds__(kPPThreads, D == 64 ? 4 : 2) void prefill_paged_attn_ppd_kernel(Params p) {
-  static_assert(D == 128 || !kTail, "the split tail tile is laid out for 256-byte rows");
   using DL = DirectLayout<D>;
   // K and V of three steps, each in its own array so that the compiler can
   // tell a read of one from a direct load in flight into another
@@ -1634,12 +1656,13 @@ __global__ __launch_bounds__(kPPThreads, D == 64 ? 4 : 2) void prefill_paged_att
   else run(std::false_type{});
 }
 
-// Launches of less than one round of ping-pong tiles, D = 128: split tiles
-// (128 rows x 8 waves over two halves of the keys) with direct-to-LDS staging.
+// Launches of less than one round of ping-pong tiles: split tiles (128 rows x
+// 8 waves over two halves of the keys) with direct-to-LDS staging.  At head
+// dim 64, 128 VGPRs and 67,584 bytes of LDS: two work-groups per CU.
 template <int D, bool kPartial>
-__global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_ppd_split_kernel(Params p) {
-  static_assert(D == 128, "direct-to-LDS staging is laid out for 256-byte rows");
-  constexpr int kBuf = 16 * (4 * D + 8);
+__global__ __launch_bounds__(kPPThreads, D == 64 ? 4 : 2) void prefill_paged_attn_ppd_split_kernel(Params p) {
+  using DL = DirectLayout<D>;
+  constexpr int kBuf = (kBN / DL::kRows) * DL::kGrp;
   __shared__ __attribute__((aligned(16))) uint16_t k0[kBuf], k1[kBuf], k2[kBuf], k3[kBuf];
   __shared__ __attribute__((aligned(16))) uint16_t v0[kBuf], v1[kBuf], v2[kBuf], v3[kBuf];
   ppd_split_tile<D, false, kPartial>(p, blockIdx.x, k0, k1, k2, k3, v0, v1, v2, v3);
@@ -1783,7 +1806,7 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
         hipLaunchKernelGGL((prefill_paged_attn_ppd_kernel<128, false>), grid, dim3(kPPThreads), 0, stream, p);
       }
     } else if (tail) {
-      hipLaunchKernelGGL((prefill_paged_attn_pp_kernel<64, true>), grid, dim3(kPPThreads), 0, stream, p);
+      hipLaunchKernelGGL((prefill_paged_attn_ppd_kernel<64, true>), grid, dim3(kPPThreads), 0, stream, p);
     } else {
       hipLaunchKernelGGL((prefill_paged_attn_ppd_kernel<64, false>), grid, dim3(kPPThreads), 0, stream, p);
     }
@@ -1792,7 +1815,7 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
     // by 8 waves over two halves of its keys
     hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<128, false>), grid, dim3(kPPThreads), 0, stream, p);
   } else {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, false, true>), grid, dim3(2 * kThreads), 0, stream, p);
+    hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<64, false>), grid, dim3(kPPThreads), 0, stream, p);
   }
   return hipGetLastError();
 }
