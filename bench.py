@@ -461,7 +461,7 @@ def bench_copy(args, dev):
     kernel, sources = {
         "decode": ("paged_decode_attn_kernel<128, false>",
                    ("paper_2608_14624_amd/csrc/paged_decode_attn.hip",)),
-        "cascade_decode": ("prefill_paged_attn_kernel<128, true, false> + paged_decode_attn_kernel<128, true>"
+        "cascade_decode": ("shared_prefix_partials_kernel<128> + paged_decode_attn_kernel<128, true>"
                            " + cascade_merge_kernel<128>",
                            ("paper_2608_14624_amd/csrc/prefill_paged_attn.hip",
                             "paper_2608_14624_amd/csrc/paged_decode_attn.hip",

@@ -117,7 +117,7 @@ struct DecodeLaunch {
 hipError_t launch_paged_decode_attn(const DecodeLaunch& a, hipStream_t stream);
 
 // Cascade decode: the shared prefix of each group of sequences is attended
-// once with the group's queries stacked (prefill kernel, stacked mode), in
+// once with the group's queries stacked (shared_prefix_partials_kernel), in
 // chunks of kCascadeChunkSteps * 64 keys whose partial results go to a
 // workspace; the decode kernel attends each sequence's own keys in segments
 // of kCascadeSegmentKeys, also as partials; a merge kernel combines them.

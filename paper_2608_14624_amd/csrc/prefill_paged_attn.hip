@@ -7,27 +7,27 @@
 // suffix row i is prompt position P + i and sees keys 0 .. P + i.
 //
 // Kernel design
-//   * One work-group = 4 wave64s = one (invocation, group of query heads that
-//     share one KV head, tile of suffix tokens).  Each wave owns 32 query rows
-//     (one head x 32 consecutive tokens), so every K/V tile staged in LDS is
-//     used by 4 waves: by 4 heads of the GQA group when the group has at
-//     least 4 heads, otherwise by consecutive token tiles of fewer heads.
+//   * Each wave owns 32 query rows (one head x 32 consecutive suffix tokens
+//     of one invocation), and the waves of a work-group share one KV head:
+//     every K/V tile staged in LDS serves several heads of its GQA group
+//     (all of them when the group has at least 4), or consecutive token
+//     tiles of fewer heads.
 //   * The contractions run on bf16 MFMA (v_mfma_f32_32x32x16_bf16) in the
 //     transposed orientation S^T = K Q^T and O^T = V^T P^T.  In that
 //     orientation a lane owns one query: the row max and row sum of the
 //     online softmax are in-lane reductions plus one exchange between the two
 //     lane halves, and the probabilities leave the S^T accumulator already in
 //     the register layout of the B operand of the PV product.
-//   * Keys are consumed 64 at a time (4 pool blocks, one staged by each
-//     wave).  K and V are both staged row-major [key][d]; the A operand of
-//     the PV product (V^T) comes from two transposing 8-byte LDS reads
-//     (ds_read_b64_tr_b16).  Rows are padded to spread LDS banks.  Block ids
-//     are read from the block table per 16-token block.
+//   * Keys are consumed 64 at a time (4 pool blocks, block ids read from the
+//     block table with scalar loads a step ahead).  K and V go from HBM
+//     straight into LDS (buffer loads with the LDS flag) as padded,
+//     XOR-swizzled [key][d] rows; the A operand of the PV product (V^T) comes
+//     from two transposing 8-byte LDS reads (ds_read_b64_tr_b16).
 //   * Masking is a select to -inf (never an additive mask), so K positions
 //     past the end of a sequence inside its last block never contribute
-//     whatever they hold; the V rows there are stored to LDS as zeros (their
-//     probabilities are 0, and 0 times a NaN would not be), and whole blocks
-//     past the end are zero-filled in LDS, never read.
+//     whatever they hold; the V rows there are overwritten with zeros in LDS
+//     (their probabilities are 0, and 0 times a NaN would not be), and whole
+//     blocks past the end are never loaded.
 //   * Softmax runs in base 2 with log2(e) folded into the scale.
 //
 // Work-group order: the KV head varies fastest, so with 8 KV heads the 8 XCDs
@@ -39,26 +39,24 @@
 // invocations' K/V in flight per XCD and ran 9% slower).
 //
 // Ping-pong kernel (launches of at least a round of its tiles): 8 waves,
-// 256 query rows per work-group, one work-group per CU, and the two waves of
-// a SIMD are offset by half a step: waves 0-3 run an iteration as [MFMAs:
-// PV of the previous step + QK^T of this one][softmax of this step], waves
-// 4-7 as [softmax of the previous step][the same MFMAs], so one wave's
-// matrix work overlaps the other's vector work between two barriers.  The
-// K/V tiles serve 8 waves instead of 4 (waves 0-3 stage K, 4-7 stage V), and
-// each row's arithmetic is the same as in the four-wave kernel, bit for bit.
-// The ppd kernels are this design with K and V loaded straight into LDS
-// (head_dim 128, and head_dim 64 launches without a split tail; at head_dim
-// 64 two work-groups share a CU).
+// 256 query rows per work-group, and the two waves of a SIMD are offset by
+// half a step: waves 0-3 run an iteration as [MFMAs: PV of the previous step
+// + QK^T of this one][softmax of this step], waves 4-7 as [softmax of the
+// previous step][the same MFMAs], so one wave's matrix work overlaps the
+// other's vector work between two barriers.  One work-group per CU at head
+// dim 128, two at 64.
 //
-// Split launches (less than a round of ping-pong tiles): a four-wave
-// tile alone on a CU would leave one wave per SIMD, with nothing to hide its
-// softmax behind.  Instead 8 waves run each 128-row tile: waves w and w + 4
-// own the same rows, waves 0-3 take the first half of the key steps and
-// waves 4-7 the second, each half with its own LDS buffers (two halves of
-// 74 KiB for D = 128), and at the end waves 4-7 hand (O, m, l) to waves 0-3
-// through LDS, which merge them with the log-sum-exp weights.  A ping-pong
-// launch whose last round would be at most half full runs that round's tiles
-// the same way, as two 128-row halves each, so it occupies every CU.
+// Split tiles (launches of less than a round of ping-pong tiles): a 128-row
+// tile of four waves alone on a CU would leave one wave per SIMD, with
+// nothing to hide its softmax behind.  Instead 8 waves run each tile: waves
+// w and w + 4 own the same rows, waves 0-3 take the first half of the key
+// steps and waves 4-7 the second, each half with its own LDS ring, and at
+// the end waves 4-7 hand (O, m, l) to waves 0-3 through LDS, which merge
+// them with the log-sum-exp weights.  A ping-pong launch whose last round
+// would be at most half full runs that round's tiles the same way, as two
+// 128-row halves each, so it occupies every CU.  Launches that leave half
+// the CUs idle even so can take a tile's keys in parts on more work-groups,
+// whose partial results a merge kernel combines (the workspace call).
 //
 // Stacked mode (the shared-prefix half of cascade attention): the query rows
 // of a work-group are any 128 (sequence, query head) pairs of one group of
@@ -66,7 +64,8 @@
 // causal limit, over one 64-key-aligned chunk of the shared prefix, and the
 // work-group writes its unnormalized partial result (O, running max m, sum
 // l) to a workspace instead of the output.  The other half (each sequence's
-// own keys) and the log-sum-exp merge run in the decode kernel.
+// own keys) and the log-sum-exp merge run in the decode kernel.  This kernel
+// stages K and V through registers into a double-buffered LDS tile.
 #include "internal.h"
 
 #include <math.h>
@@ -215,14 +214,11 @@ __device__ __forceinline__ float pair_sum(float x) {
 
 constexpr int kRowsPerWG = kNQ * kWaves;
 
-// kSplit: 8 waves; waves w and w + 4 own the same 32 rows, waves 0-3 take
-// the first half of the key steps and waves 4-7 the second, each half with
-// its own LDS buffers; the halves are merged through LDS at the end.  For
-// launches too small for two work-groups per CU, and for the tail of a
-// ping-pong launch (kTail: work-group wg takes one half of a ping-pong tile).
-template <int D, bool kStacked, bool kSplit, bool kTail>
-__device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const int wg) {
-  static_assert(!kTail || (kSplit && !kStacked), "a tail tile runs split");
+// One 128-row tile of stacked rows against one chunk of a group's shared
+// prefix: four waves of 32 rows, K and V staged through two register stages
+// into a double-buffered LDS tile; writes the chunk's partial result.
+template <int D>
+__device__ __forceinline__ void stacked_tile(const Params& p, Lds<D>& sm, const int wg) {
   constexpr int kStride = Lds<D>::kStride;
   constexpr int vStride = Lds<D>::vStride;
   constexpr int KS = D / 16;     // MFMA k-steps over the head dim
@@ -230,104 +226,39 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = (tid >> 6) & 3;            // row owner within the work-group
-  const int split_half = kSplit ? __builtin_amdgcn_readfirstlane(tid >> 8) : 0;
-  Lds<D>& sm = sm_all[split_half];
+  const int wave = tid >> 6;                  // row owner within the work-group
   const int qi = lane & 31;
   const int half = lane >> 5;
 
   // ---- work tile -----------------------------------------------------
   // Work-groups are dealt to the 8 XCDs round-robin, so the KV head is the
-  // fastest-varying index: with 8 KV heads every XCD serves exactly one and
-  // keeps its K/V in its own L2.
-  int g;                // KV head
-  bool row_valid;       // this lane holds a real query row
-  size_t qrow;          // element offset of the row in q (and out)
-  int qpos;             // last key the row sees
-  int j0;               // first 64-key step
-  int n_steps;          // steps of the work-group
-  int n_blk;            // blocks of the key range reached through bt
-  int kv_len;           // keys of the sequence (V rows from there on are zeroed)
-  int wave_qmin;        // first key position some row of this wave cannot see
-  const int32_t* bt;
-  int chunk = 0;
-  if constexpr (!kStacked) {
-    // the head tiles of the KV head come next, then the token tiles of an
-    // invocation from the last (most keys) to the first, then invocations
-    const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
-    int tile = wg;
-    int span = p.span;
-    int sub_half = 0;
-    if constexpr (kTail) {
-      // halves of one ping-pong tile are num_kv_heads work-groups apart,
-      // so both run on the XCD that holds their KV head
-      const long long j = wg - p.pp_grid;
-      const int kv = (int)(j % p.num_kv_heads);
-      const long long rj = j / p.num_kv_heads;
-      sub_half = (int)(rj & 1);
-      tile = (int)(p.pp_grid + (rj >> 1) * p.num_kv_heads + kv);
-      span = p.span / 2;
-    }
-    g = tile % p.num_kv_heads;
-    const int sub = tile / p.num_kv_heads;
-    const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
-    const int rest = sub / tiles_per_kv;
-    const int r = rest / p.token_tiles;
-    const int token_tile = p.token_tiles - 1 - rest % p.token_tiles;
-    const int q0 = p.cu_q_lens[r];
-    const int S = p.cu_q_lens[r + 1] - q0;
-    const int t0 = token_tile * p.span + sub_half * span;
-    if (t0 >= S) return;
-    const int P = p.prefix_lens[r];
-    const int L = P + S;
-    const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
-    const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
-    row_valid = t < S;
-    qrow = ((size_t)(q0 + (row_valid ? t : 0)) * p.num_q_heads + h) * D;
-    qpos = row_valid ? P + t : L - 1;
-    const int kv_end = P + min(S, t0 + span);                // keys the tile needs
-    j0 = 0;
-    n_steps = (kv_end + kBN - 1) / kBN;
-    n_blk = (L + kBlock - 1) / kBlock;
-    kv_len = L;
-    bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
-    wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
-  } else {
-    // then row tiles, chunks of the shared prefix, groups
-    g = wg % p.num_kv_heads;
-    int rest = wg / p.num_kv_heads;
-    const int rt = rest % p.row_tiles;
-    rest /= p.row_tiles;
-    chunk = rest % p.chunks;
-    const int gr = rest / p.chunks;
-    const int s0 = p.cu_groups[gr];
-    const int n_rows = (p.cu_groups[gr + 1] - s0) * p.group;
-    const int SH = p.shared_lens[gr];
-    const int kb = chunk * p.chunk_steps * kBN;
-    if (rt * kRowsPerWG >= n_rows || kb >= SH) return;
-    const int ke = min(SH, kb + p.chunk_steps * kBN);
-    const int rho = rt * kRowsPerWG + wave * kNQ + qi;
-    row_valid = rho < n_rows;
-    const int rr = row_valid ? rho : 0;
-    const int seq = s0 + rr / p.group;
-    const int h = g * p.group + rr % p.group;
-    qrow = ((size_t)seq * p.num_q_heads + h) * D;
-    qpos = ke - 1;
-    j0 = kb / kBN;
-    n_steps = (ke - kb + kBN - 1) / kBN;
-    n_blk = SH / kBlock;
-    kv_len = SH;                                              // whole blocks
-    bt = p.block_tables + (size_t)s0 * p.max_blocks_per_seq;   // the group's shared blocks
-    wave_qmin = ke - 1;
-  }
-  // split mode: this half's steps; both halves run n_iter iterations so
-  // that their barriers match
-  const int n_iter = kSplit ? n_steps - n_steps / 2 : n_steps;
-  if constexpr (kSplit) {
-    const int first = split_half ? n_steps / 2 : 0;
-    n_steps = split_half ? n_steps - n_steps / 2 : n_steps / 2;
-    j0 += first;
-  }
+  // fastest-varying index (with 8 KV heads every XCD serves exactly one and
+  // keeps its K/V in its own L2); then row tiles, chunks of the shared
+  // prefix, groups.  Stacked row rho of a group is query head
+  // g * group + rho % group of its sequence rho / group.
+  const int g = wg % p.num_kv_heads;
+  int rest = wg / p.num_kv_heads;
+  const int rt = rest % p.row_tiles;
+  rest /= p.row_tiles;
+  const int chunk = rest % p.chunks;
+  const int gr = rest / p.chunks;
+  const int s0 = p.cu_groups[gr];
+  const int n_rows = (p.cu_groups[gr + 1] - s0) * p.group;
+  const int SH = p.shared_lens[gr];
+  const int kb = chunk * p.chunk_steps * kBN;
+  if (rt * kRowsPerWG >= n_rows || kb >= SH) return;
+  const int ke = min(SH, kb + p.chunk_steps * kBN);
+  const int qpos = ke - 1;                               // every row sees the whole chunk
+  const int rho = rt * kRowsPerWG + wave * kNQ + qi;
+  const bool row_valid = rho < n_rows;                   // this lane holds a real row
+  const int rr = row_valid ? rho : 0;
+  const int seq = s0 + rr / p.group;
+  const int h = g * p.group + rr % p.group;
+  const size_t qrow = ((size_t)seq * p.num_q_heads + h) * D;   // element offset in q
+  const int j0 = kb / kBN;                               // first 64-key step
+  const int n_steps = (ke - kb + kBN - 1) / kBN;
+  const int n_blk = SH / kBlock;                         // shared prefixes are whole blocks
+  const int32_t* bt = p.block_tables + (size_t)s0 * p.max_blocks_per_seq;   // the group's shared blocks
   const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
   const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
   const uint16_t* kbase = p.k_pool + (size_t)g * tile_elems;
@@ -387,21 +318,6 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
       *reinterpret_cast<uint4*>(&buf[key * stride + (c % kChunksPerRow) * 8]) = src[u];
     }
   };
-  // V rows past the end of the sequence inside its last block (key0: the
-  // block's first key) are overwritten with zeros after the block is
-  // stored: their probabilities are 0, but 0 times a stale NaN or Inf in the
-  // pool is NaN.  Only the one block that holds the end takes this path.
-  auto zero_tail = [&](uint16_t* buf, int key0) {
-    if (!kStacked && key0 < kv_len && key0 + kBlock > kv_len) {   // shared prefixes: whole blocks
-#pragma unroll
-      for (int u = 0; u < kKLoads; ++u) {
-        const int c = lane + 64 * u;
-        if (key0 + c / kChunksPerRow >= kv_len)
-          *reinterpret_cast<uint4*>(&buf[(wave_u * kBlock + c / kChunksPerRow) * vStride +
-                                         (c % kChunksPerRow) * 8]) = make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
   // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
   // transposing reads.  ds_read_b64_tr_b16 treats the 8-byte rows addressed
   // by the 16 lanes of a group as a 16 x 4 matrix M and hands lane j of the
@@ -447,7 +363,6 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
     load_tile(vreg[0], vbase, id0);
     store_tile(kreg[0], sm.k[0], kStride);
     store_tile(vreg[0], sm.v[0], vStride);
-    zero_tail(sm.v[0], j0 * kBN + wave_u * kBlock);
     if (n_steps > 1) {
       const int id1 = block_id(1);
       load_tile(kreg[1], kbase, id1);
@@ -467,11 +382,9 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
     const int kstart = (j0 + j) * kBN;
     const int cur = j & 1;
     __syncthreads();   // iteration j-1's reads are done and its writes visible
-    if (kSplit && j >= n_steps) return;            // this half is done; keep the barriers
     if (j + 1 < n_steps) {
       store_tile(kst, sm.k[cur ^ 1], kStride);     // K_{j+1}, V_{j+1}
       store_tile(vst, sm.v[cur ^ 1], vStride);
-      zero_tail(sm.v[cur ^ 1], kstart + kBN + wave_u * kBlock);
     }
     if (j + 3 < n_steps) {                          // in flight for two steps
       load_tile(kst, kbase, id_next);
@@ -488,10 +401,10 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
     logits(sm.k[cur], s_cur);
     __builtin_amdgcn_s_setprio(0);
 
-    // ---- mask (only where some key of the step is past a row's limit) --
+    // ---- mask: keys past the chunk's end (a last step that is not full)
     // accumulator register rr of tile mt holds key
     //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
-    if (kstart + kBN - 1 > wave_qmin) {
+    if (kstart + kBN - 1 > qpos) {
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -510,12 +423,10 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
     mloc = pair_max(mloc);
     // ---- lazy rescale: move the reference max only when a row's max grew
     // by more than 2^8 in probability; otherwise keep it (p <= 256 then)
-    // (a row whose keys so far were all masked keeps m_run = -inf: possible
-    // only for the second half of a split work-group)
     const bool grow = (mloc - m_run) * c > 8.f;      // true for every row at step 0
     if (__builtin_amdgcn_ballot_w64(grow) != 0) {
       const float m_new = grow ? mloc : m_run;
-      const float alpha = (kSplit && m_new == m_run) ? 1.f : __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
       m_run = m_new;
 #pragma unroll
       for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
@@ -523,7 +434,7 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
       for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
     }
 
-    const float mc = (kSplit && m_run == -INFINITY) ? 0.f : m_run * c;
+    const float mc = m_run * c;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -556,410 +467,34 @@ __device__ __forceinline__ void attn_tile(const Params& p, Lds<D>* sm_all, const
   };
 
   // unrolled by two so the register stage of each step is a constant
-  for (int j = 0; j < n_iter; j += 2) {
+  for (int j = 0; j < n_steps; j += 2) {
     step(j, kreg[1], vreg[1]);
-    if (j + 1 < n_iter) step(j + 1, kreg[0], vreg[0]);
+    if (j + 1 < n_steps) step(j + 1, kreg[0], vreg[0]);
   }
   const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
 
-  float l_tot = pair_sum(l_run);
-  if constexpr (kSplit) {
-    // waves 4-7 hand (O, m, l) of their rows to waves 0-3 through the second
-    // half's LDS, which every wave has finished reading; value e of lane l
-    // of wave w sits at word e * 256 + 64 w + l (no bank conflicts)
-    constexpr int kX = DT * 16 + 2;
-    static_assert(kX * 256 * sizeof(float) <= sizeof(Lds<D>), "exchange exceeds one LDS half");
-    float* x = reinterpret_cast<float*>(&sm_all[kSplit ? 1 : 0]) + wave * 64 + lane;
-    __syncthreads();
-    if (split_half == 1) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) x[(dt * 16 + rr) * 256] = oacc[dt][rr];
-      x[DT * 16 * 256] = m_run;
-      x[(DT * 16 + 1) * 256] = l_tot;
-    }
-    __syncthreads();
-    if (split_half == 1) return;
-    const float m1 = x[DT * 16 * 256];
-    const float mx = fmaxf(m_run, m1);
-    const float w0 = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run - mx) * c);
-    const float w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m1 - mx) * c);
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int rr = 0; rr < 16; ++rr) oacc[dt][rr] = w0 * oacc[dt][rr] + w1 * x[(dt * 16 + rr) * 256];
-    l_tot = w0 * l_tot + w1 * x[(DT * 16 + 1) * 256];
-  }
-  if constexpr (kStacked) {
-    // ---- partial result: O (relative to m_run), m_run, l -----------
-    if (row_valid) {
-      const size_t widx = (size_t)chunk * p.ws_rows + qrow / D;
-      float* orow = p.ws_o + widx * D;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-          const float4 o = make_float4(oacc[dt][rg * 4], oacc[dt][rg * 4 + 1], oacc[dt][rg * 4 + 2],
-                                       oacc[dt][rg * 4 + 3]);
-          *reinterpret_cast<float4*>(orow + dt * 32 + 8 * rg + 4 * half) = o;
-        }
-      }
-      if (half == 0) *reinterpret_cast<float2*>(p.ws_ml + 2 * widx) = make_float2(m_run, l_tot);
-    }
-    return;
-  }
-  // ---- epilogue: O / l, bf16, store --------------------------------
-  const float inv = 1.f / l_tot;
+  const float l_tot = pair_sum(l_run);
+  // ---- partial result: O (relative to m_run), m_run, l ---------------
   if (row_valid) {
-    uint16_t* orow = p.out + qrow;
+    const size_t widx = (size_t)chunk * p.ws_rows + qrow / D;
+    float* orow = p.ws_o + widx * D;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        bf16x4 o;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) o[u] = (__bf16)(oacc[dt][rg * 4 + u] * inv);
-        *reinterpret_cast<uint2*>(orow + dt * 32 + 8 * rg + 4 * half) = __builtin_bit_cast(uint2, o);
+        const float4 o = make_float4(oacc[dt][rg * 4], oacc[dt][rg * 4 + 1], oacc[dt][rg * 4 + 2],
+                                     oacc[dt][rg * 4 + 3]);
+        *reinterpret_cast<float4*>(orow + dt * 32 + 8 * rg + 4 * half) = o;
       }
     }
+    if (half == 0) *reinterpret_cast<float2*>(p.ws_ml + 2 * widx) = make_float2(m_run, l_tot);
   }
 }
 
-template <int D, bool kStacked, bool kSplit>
-__global__ __launch_bounds__(kSplit ? 2 * kThreads : kThreads) void prefill_paged_attn_kernel(Params p) {
-  __shared__ Lds<D> sm_all[kSplit ? 2 : 1];
-  attn_tile<D, kStacked, kSplit, false>(p, sm_all, blockIdx.x);
-}
-
-// kTail: ping-pong tiles below pp_grid; the tail of the launch (at most half
-// a round of ping-pong tiles) runs as twice as many half tiles on the split
-// path, which fills the last round's idle CUs.  LDS: the split path's two
-// halves; a ping-pong tile uses the first.  Launches without a tail take the
-// plain kernel (one LDS half).  D = 128 runs the direct-to-LDS kernel below
-// instead.  The ping-pong body stays in the kernel
-// itself: moved into a device function, it compiled to more registers and
-// ran 3-5% slower.
-template <int D, bool kTail>
-__global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Params p) {
-  static_assert(kPPThreads == 2 * kThreads, "the split tail runs 8 waves too");
-  __shared__ Lds<D> sm_all[kTail ? 2 : 1];
-  Lds<D>& sm = sm_all[0];
-  const int wg = blockIdx.x;
-  if constexpr (kTail) {
-    if (wg >= p.pp_grid) {
-      attn_tile<D, false, true, true>(p, sm_all, wg);
-      return;
-    }
-  }
-  constexpr int kStride = Lds<D>::kStride;
-  constexpr int vStride = Lds<D>::vStride;
-  constexpr int KS = D / 16;     // MFMA k-steps over the head dim
-  constexpr int DT = D / 32;     // 32-wide output tiles over the head dim
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int qi = lane & 31;
-  const int half = lane >> 5;
-  // group A (waves 0-3) runs MFMA-first, group B (waves 4-7) VALU-first; the
-  // two waves of a SIMD belong to different groups
-  const bool group_b = __builtin_amdgcn_readfirstlane(wave) >= 4;
-
-  // ---- work tile (same order as the four-wave kernel) -----------------
-  const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
-  const int g = wg % p.num_kv_heads;
-  const int sub = wg / p.num_kv_heads;
-  const int head_tile = g * tiles_per_kv + sub % tiles_per_kv;
-  const int rest = sub / tiles_per_kv;
-  const int r = rest / p.token_tiles;
-  const int token_tile = p.token_tiles - 1 - rest % p.token_tiles;
-  const int q0 = p.cu_q_lens[r];
-  const int S = p.cu_q_lens[r + 1] - q0;
-  const int t0 = token_tile * p.span;
-  if (t0 >= S) return;
-  const int P = p.prefix_lens[r];
-  const int L = P + S;
-  const int h = head_tile * p.heads_per_wg + wave % p.heads_per_wg;
-  const int t = t0 + (wave / p.heads_per_wg) * kNQ + qi;   // this lane's suffix row
-  const bool row_valid = t < S;
-  const size_t qrow = ((size_t)(q0 + (row_valid ? t : 0)) * p.num_q_heads + h) * D;
-  const int qpos = row_valid ? P + t : L - 1;               // last visible key
-  const int kv_end = P + min(S, t0 + p.span);               // keys the tile needs
-  const int n_steps = (kv_end + kBN - 1) / kBN;
-  const int n_blk = (L + kBlock - 1) / kBlock;
-  const int32_t* bt = p.block_tables + (size_t)r * p.max_blocks_per_seq;
-  // first key position some row of this wave cannot see
-  const int wave_qmin = P + min(t0 + (wave / p.heads_per_wg) * kNQ, S - 1);
-  const size_t tile_elems = (size_t)kBlock * D;             // one (block, head)
-  const size_t slot_elems = (size_t)p.num_kv_heads * tile_elems;
-
-  // ---- Q^T operand: lane holds query qi, dims ks*16 + half*8 .. +7 -----
-  bf16x8 qreg[KS];
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (row_valid) v = *reinterpret_cast<const uint4*>(p.q + qrow + ks * 16 + half * 8);
-    qreg[ks] = as_bf16x8(v);
-  }
-
-  // ---- staging: waves 0-3 move K, waves 4-7 move V; wave w moves pool block
-  // 4*step + (w & 3).  K is staged for the step the next iteration's logits
-  // use, V for the step whose probabilities the next iteration multiplies.
-  constexpr int kChunksPerRow = D / 8;
-  constexpr int kKLoads = kBlock * kChunksPerRow / 64;             // 4 (D=128), 2 (D=64)
-  const int slot_u = __builtin_amdgcn_readfirstlane(wave & 3);
-  const uint16_t* my_base = (group_b ? p.v_pool : p.k_pool) + (size_t)g * tile_elems;
-  const __attribute__((address_space(4))) int32_t* bt_c =
-      (const __attribute__((address_space(4))) int32_t*)bt;
-  auto block_id = [&](int step) __attribute__((always_inline)) -> int {
-    const int lb = step * (kBN / kBlock) + slot_u;
-    return (step < n_steps && lb < n_blk) ? bt_c[lb] : -1;          // -1: past the end
-  };
-  using Stage = uint4[kKLoads];
-  uint4 stage[2][kKLoads];
-  auto load_tile_at = [&](Stage& dst, const uint16_t* src, int id) __attribute__((always_inline)) {
-    if (id >= 0) {
-#pragma unroll
-      for (int u = 0; u < kKLoads; ++u) {
-        const int c = lane + 64 * u;
-        dst[u] = *reinterpret_cast<const uint4*>(src + (c / kChunksPerRow) * D + (c % kChunksPerRow) * 8);
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < kKLoads; ++u) dst[u] = make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto load_tile = [&](Stage& dst, int id) __attribute__((always_inline)) {
-    load_tile_at(dst, my_base + (size_t)(id >= 0 ? id : 0) * slot_elems, id);
-  };
-  auto store_tile = [&](const Stage& src, uint16_t* dst, int stride) __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < kKLoads; ++u) {
-      const int c = lane + 64 * u;
-      const int key = slot_u * kBlock + c / kChunksPerRow;
-      *reinterpret_cast<uint4*>(&dst[key * stride + (c % kChunksPerRow) * 8]) = src[u];
-    }
-  };
-  // V rows past the end of the sequence inside its last block (key0: the
-  // block's first key) are overwritten with zeros after the block is stored
-  // (probabilities 0 times a stale NaN or Inf would be NaN); only the block
-  // that holds the end takes this path.
-  auto zero_tail = [&](uint16_t* dst, int key0) __attribute__((always_inline)) {
-    if (key0 < L && key0 + kBlock > L) {
-#pragma unroll
-      for (int u = 0; u < kKLoads; ++u) {
-        const int c = lane + 64 * u;
-        if (key0 + c / kChunksPerRow >= L)
-          *reinterpret_cast<uint4*>(&dst[(slot_u * kBlock + c / kChunksPerRow) * vStride +
-                                         (c % kChunksPerRow) * 8]) = make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  // V^T fragment for keys 16*ks2 .. +15 and dims 32*dt .. +31 from two
-  // transposing reads (ds_read_b64_tr_b16: lane j of a 16-lane group gets
-  // M[4e + j/4][j%4] of the 8-byte rows its lanes address).
-  const int tr_row = 4 * (lane >> 5) + ((lane & 15) >> 2);
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  auto v_frag = [&](const uint16_t* vbuf, int ks2, int dt) __attribute__((always_inline)) -> bf16x8 {
-    const uint16_t* base = &vbuf[(16 * ks2 + tr_row) * vStride + 32 * dt + tr_col];
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + 8 * vStride));
-    const i16x4 lohi[2] = {lo, hi};
-    return __builtin_bit_cast(bf16x8, lohi);
-  };
-
-  auto run = [&](auto group_tag) __attribute__((always_inline)) {
-    constexpr bool kB = decltype(group_tag)::value;
-    f32x16 oacc[DT];
-  #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x16{};
-    f32x16 s_acc[2];             // logits of the step whose softmax is pending
-    bf16x8 pb[kBN / 16];         // probabilities of the step whose PV is pending
-    float m_run = -INFINITY;     // running max of the raw (unscaled) logits
-    float l_part[4] = {0.f, 0.f, 0.f, 0.f};
-    const float c = p.scale_log2;
-
-    // M phase of iteration j: O += P_{j-1} V_{j-1}, then S_j = K_j Q^T
-    auto mfma_phase = [&](int j) __attribute__((always_inline)) {
-      __builtin_amdgcn_s_setprio(1);
-      if (j >= 1) {
-        const uint16_t* vbuf = sm.v[(j - 1) & 1];
-  #pragma unroll
-        for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
-  #pragma unroll
-          for (int dt = 0; dt < DT; ++dt)
-            oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v_frag(vbuf, ks2, dt), pb[ks2], oacc[dt], 0, 0, 0);
-        }
-        // interleave, the reads one 16-key slice ahead of their MFMAs
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
-#pragma unroll
-        for (int ks2 = 1; ks2 < kBN / 16; ++ks2) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 2 * DT, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, DT, 0);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      if (j < n_steps) {
-        const uint16_t* kbuf = sm.k[j & 1];
-        s_acc[0] = f32x16{};
-        s_acc[1] = f32x16{};
-  #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-  #pragma unroll
-          for (int mt = 0; mt < 2; ++mt) {
-            const uint4 a = *reinterpret_cast<const uint4*>(&kbuf[(mt * 32 + qi) * kStride + ks * 16 + half * 8]);
-            s_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), qreg[ks], s_acc[mt], 0, 0, 0);
-          }
-        }
-        __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
-#pragma unroll
-        for (int ks = 2; ks < KS; ++ks) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
-          __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
-      }
-      __builtin_amdgcn_s_setprio(0);
-    };
-
-    // V phase for step x: mask, online softmax, P_x in bf16, row sums
-    auto valu_phase = [&](int x) __attribute__((always_inline)) {
-      if (x < 0 || x >= n_steps) return;
-      const int kstart = x * kBN;
-      // accumulator register rr of tile mt holds key
-      //   kstart + 32*mt + 8*(rr/4) + 4*half + rr%4   for query qi
-      if (kstart + kBN - 1 > wave_qmin) {
-  #pragma unroll
-        for (int mt = 0; mt < 2; ++mt) {
-  #pragma unroll
-          for (int rr = 0; rr < 16; ++rr) {
-            const int kj = kstart + mt * 32 + 8 * (rr >> 2) + 4 * half + (rr & 3);
-            s_acc[mt][rr] = (kj <= qpos) ? s_acc[mt][rr] : -INFINITY;
-          }
-        }
-      }
-      float mloc = -INFINITY;
-  #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) {
-  #pragma unroll
-        for (int rr = 0; rr < 16; ++rr) mloc = fmaxf(mloc, s_acc[mt][rr]);
-      }
-      mloc = pair_max(mloc);
-      // lazy rescale: move the reference max only when a row's max grew by
-      // more than 2^8 in probability (true for every row at the first step)
-      const bool grow = (mloc - m_run) * c > 8.f;
-      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
-        const float m_new = grow ? mloc : m_run;
-        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
-        m_run = m_new;
-  #pragma unroll
-        for (int u = 0; u < 4; ++u) l_part[u] *= alpha;
-  #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
-      }
-      const float mc = m_run * c;
-      const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-  #pragma unroll
-      for (int ks2 = 0; ks2 < kBN / 16; ++ks2) {
-        const int mt = ks2 >> 1;
-        const int rb = (ks2 & 1) * 8;
-  #pragma unroll
-        for (int s2 = 0; s2 < 8; ++s2)
-          pb[ks2][s2] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s_acc[mt][rb + s2], c, -mc));
-        // row sum over the same bf16 probabilities the PV product uses
-        l_part[0] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 0, 1), ones, l_part[0], false);
-        l_part[1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 2, 3), ones, l_part[1], false);
-        l_part[2] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 4, 5), ones, l_part[2], false);
-        l_part[3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[ks2], pb[ks2], 6, 7), ones, l_part[3], false);
-      }
-    };
-
-    // ---- prologue ------------------------------------------------------
-    // K waves: K_0 into LDS, K_1 and K_2 in registers; V waves: V_0 and V_1
-    // in registers (V_j is stored at iteration j, K_{j+1} at iteration j).
-    int id_next;     // block of the step the next iteration loads, read ahead
-    if (!kB) {
-      load_tile(stage[0], block_id(0));
-      store_tile(stage[0], sm.k[0], kStride);
-      load_tile(stage[1], block_id(1));
-      load_tile(stage[0], block_id(2));
-      id_next = block_id(3);
-    } else {
-      load_tile(stage[0], block_id(0));
-      load_tile(stage[1], block_id(1));
-      id_next = block_id(2);
-    }
-
-    // One iteration: stage data for the next iteration, then the two phases in
-    // group order.  Iteration j reads K_j and V_{j-1}; it stores K_{j+1} into
-    // the K buffer K_{j-1} used and V_j into the V buffer V_{j-2} used, both
-    // read in iteration j-1, before this iteration's barrier.
-    auto iteration = [&](const int j, Stage& st) __attribute__((always_inline)) {
-      __syncthreads();
-      // the scalar read of the block id is waited for here, before this
-      // iteration's LDS stores, so the wait does not include them
-      const int id = id_next;
-      const uint16_t* src = my_base + (size_t)(id >= 0 ? id : 0) * slot_elems;
-      __builtin_amdgcn_sched_barrier(0);
-      if (!kB) {
-        if (j + 1 < n_steps) store_tile(st, sm.k[(j + 1) & 1], kStride);
-        if (j + 3 < n_steps) load_tile_at(st, src, id);
-      } else {
-        if (j < n_steps) {
-          store_tile(st, sm.v[j & 1], vStride);
-          zero_tail(sm.v[j & 1], j * kBN + slot_u * kBlock);
-        }
-        if (j + 2 < n_steps) load_tile_at(st, src, id);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      if (!kB) {
-        mfma_phase(j);
-        __builtin_amdgcn_sched_barrier(0);
-        valu_phase(j);
-      } else {
-        valu_phase(j - 1);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_phase(j);
-      }
-      // the next iteration's block id, read once this iteration's LDS reads
-      // have been consumed
-      __builtin_amdgcn_sched_barrier(0);
-      id_next = block_id(kB ? j + 3 : j + 4);
-    };
-    // register stage of iteration j: K waves stage[(j+1)&1] (K_{j+1} is
-    // stored, K_{j+3} loaded), V waves stage[j&1] (V_j stored, V_{j+2} loaded);
-    // unrolled by two so the stage is a constant
-    for (int j = 0; j <= n_steps; j += 2) {
-      if (!kB) {
-        iteration(j, stage[1]);
-        if (j + 1 <= n_steps) iteration(j + 1, stage[0]);
-      } else {
-        iteration(j, stage[0]);
-        if (j + 1 <= n_steps) iteration(j + 1, stage[1]);
-      }
-    }
-    const float l_run = (l_part[0] + l_part[1]) + (l_part[2] + l_part[3]);
-    const float l_tot = pair_sum(l_run);
-    const float inv = 1.f / l_tot;
-    if (row_valid) {
-      uint16_t* orow = p.out + qrow;
-  #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-  #pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-          bf16x4 o;
-  #pragma unroll
-          for (int u = 0; u < 4; ++u) o[u] = (__bf16)(oacc[dt][rg * 4 + u] * inv);
-          *reinterpret_cast<uint2*>(orow + dt * 32 + 8 * rg + 4 * half) = __builtin_bit_cast(uint2, o);
-        }
-      }
-    }
-
-  };
-  if (group_b) run(std::true_type{});
-  else run(std::false_type{});
+template <int D>
+__global__ __launch_bounds__(kThreads) void shared_prefix_partials_kernel(Params p) {
+  __shared__ Lds<D> sm;
+  stacked_tile<D>(p, sm, blockIdx.x);
 }
 
 // Split tile with direct-to-LDS staging: 8 waves over one tile of span rows
@@ -969,8 +504,9 @@ __global__ __launch_bounds__(kPPThreads) void prefill_paged_attn_pp_kernel(Param
 // second; each wave loads one block of K and one of V per step straight into
 // a two-deep ring of its half (k0/k1, v0/v1 or k2/k3, v2/v3), one iteration
 // ahead (an iteration takes about 2 us, ample for a load), and the halves
-// merge through LDS at the end.  The arithmetic is that of the split path of
-// the four-wave kernel, in the same order.
+// merge through LDS at the end.  Per step the arithmetic of a row is that of
+// the ping-pong kernel (logits, mask, lazy rescale, exp2, bf16 P, row sums
+// over the same bf16 values, PV), in the same order.
 template <int D, bool kTailTile, bool kPartial = false>
 __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, uint16_t* k0, uint16_t* k1,
                                                uint16_t* k2, uint16_t* k3, uint16_t* v0, uint16_t* v1,
@@ -988,9 +524,9 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   const int qi = lane & 31;
   const int half = lane >> 5;
 
-  // ---- work tile (the order of the four-wave kernel); the halves of a
-  // ping-pong tile are num_kv_heads work-groups apart, so both run on the
-  // XCD that holds their KV head
+  // ---- work tile (the order of the ping-pong kernel, with 128-row tiles);
+  // the halves of a ping-pong tile are num_kv_heads work-groups apart, so
+  // both run on the XCD that holds their KV head
   const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
   int tile = wg;
   int sub_half = 0;
@@ -1309,12 +845,11 @@ __device__ __forceinline__ void ppd_split_tile(const Params& p, const int wg, ui
   }
 }
 
-// The ping-pong kernel with direct-to-LDS staging (D = 128 and 64): no
-// round trip through registers, so the staging registers per lane go, and
-// the loads of a step have two iterations to land in a three-deep ring of K
-// and V buffers.  Same arithmetic in the same order as the ping-pong kernel,
-// so the results are bitwise equal.  kTail: as in the ping-pong kernel, the
-// work-groups from pp_grid on take half tiles of the launch's last round.
+// The ping-pong kernel (D = 128 and 64).  K and V go straight from HBM into
+// LDS, with no round trip through registers, and the loads of a step have
+// two iterations to land in a three-deep ring of K and V buffers.  kTail:
+// the work-groups from pp_grid on take the 128-row halves of the tiles of
+// the launch's last round (split tiles).
 // At head_dim 64 the kernel holds at most 128 VGPRs (at least four waves per
 // SIMD) and 50,688 bytes of LDS (67,584 with the tail's two more buffers),
 // so two work-groups share a CU.
@@ -1347,7 +882,8 @@ __global__ __launch_bounds__(kPPThreads, D == 64 ? 4 : 2) void prefill_paged_att
   // two waves of a SIMD belong to different groups
   const bool group_b = __builtin_amdgcn_readfirstlane(wave) >= 4;
 
-  // ---- work tile (same order as the four-wave kernel) -----------------
+  // ---- work tile: KV head fastest, then head tiles, then token tiles from
+  // the last to the first, then invocations
   const int tiles_per_kv = p.head_tiles / p.num_kv_heads;
   const int g = wg % p.num_kv_heads;
   const int sub = wg / p.num_kv_heads;
@@ -1857,9 +1393,9 @@ hipError_t launch_shared_prefix_partials(const CascadeLaunch& a, hipStream_t str
   p.ws_rows = a.batch * a.num_q_heads;
   const dim3 grid((unsigned)geo.grid), block(kThreads);
   if (a.head_dim == 128) {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<128, true, false>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((shared_prefix_partials_kernel<128>), grid, block, 0, stream, p);
   } else {
-    hipLaunchKernelGGL((prefill_paged_attn_kernel<64, true, false>), grid, block, 0, stream, p);
+    hipLaunchKernelGGL((shared_prefix_partials_kernel<64>), grid, block, 0, stream, p);
   }
   return hipGetLastError();
 }
