@@ -150,14 +150,14 @@ int cs_prefill_paged_attn(const void *q, const void *k_pool, const void *v_pool,
  * When a call of cs_prefill_paged_attn would run its split kernel on at most
  * half as many 128-row tiles as there are compute units, this call cuts
  * every tile's key steps into `parts` contiguous pieces (2 to 4: as many as
- * fit one round of one work-group per CU, at most half the key steps of the
- * longest sequence) that run on separate work-groups; each writes its rows'
- * partial result (O relative to its running maximum m, m, and the
- * probability sum l, in fp32) to the workspace, and a second kernel combines
- * the parts of every (token, query head) row with log-sum-exp weights into
- * the bf16 output.  The result equals cs_prefill_paged_attn's up to rounding
- * order.  Other launches (head_dim 64, more tiles) ignore the workspace and
- * run exactly as cs_prefill_paged_attn.
+ * fit one round of one work-group per CU, each at least four 64-key steps
+ * of the longest sequence, which must have at least 16) that run on
+ * separate work-groups; each writes its rows' partial result (O relative to
+ * its running maximum m, m, and the probability sum l, in fp32) to the
+ * workspace, and a second kernel combines the parts of every (token, query
+ * head) row with log-sum-exp weights into the bf16 output.  The result
+ * equals cs_prefill_paged_attn's up to rounding order.  Other launches (more tiles, or fewer than 16 key steps) ignore
+ * the workspace and run exactly as cs_prefill_paged_attn.
  *
  * Arguments as in cs_prefill_paged_attn, plus
  *   workspace        device, 16-byte aligned, caller-owned scratch of at least

@@ -28,8 +28,12 @@ struct AttnLaunch {
   void* workspace;    // null: no key parts (see attn_geometry)
 };
 
-// most key parts a split launch takes (work-groups per tile)
+// most key parts a split launch takes (work-groups per tile), the fewest
+// 64-key steps of the longest sequence per part, and the fewest steps of
+// the longest sequence for a launch to take parts at all
 constexpr int kMaxKeyParts = 4;
+constexpr int kMinPartSteps = 4;
+constexpr int kMinPartedSteps = 16;
 
 // Compute units of the caller's current device, read from the runtime once
 // per device and cached (a host-only query, safe during stream capture).
@@ -55,7 +59,7 @@ struct AttnGeometry {
 // any other count of XCDs changes only which L2 serves a tile, not the result.
 // allow_parts: the caller gave a workspace, so a split launch that would
 // leave at least half the CUs idle takes its tiles' keys in up to
-// kMaxKeyParts parts on separate work-groups (head_dim 128), whose partials
+// kMaxKeyParts parts on separate work-groups, whose partials
 // a merge kernel combines.
 AttnGeometry attn_geometry(int batch, int max_q_len, int max_kv_len, int num_q_heads, int num_kv_heads,
                            int head_dim, int cus, bool allow_parts);

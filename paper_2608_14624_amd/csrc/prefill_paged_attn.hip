@@ -1268,17 +1268,20 @@ AttnGeometry attn_geometry(int batch, int max_q_len, int max_kv_len, int num_q_h
     geo.grid = (long long)geo.token_tiles * batch * geo.head_tiles;
     geo.pp_grid = 0;
     geo.split_tiles = geo.grid;
-    // with a workspace (D = 128), a launch that leaves at least half the CUs
-    // idle cuts each tile's keys into parts on separate work-groups, as many
-    // as fit one round (at most kMaxKeyParts), each part at least two steps
-    // of the longest sequence so that both key halves of a part have work.
+    // with a workspace, a launch that leaves at least half the CUs idle and
+    // whose longest sequence has at least kMinPartedSteps key steps cuts each
+    // tile's keys into parts on separate work-groups, as many as fit one
+    // round (at most kMaxKeyParts), each part at least kMinPartSteps steps of
+    // the longest sequence.  (Single small launches of 5-12 steps ran 0.4-1.5
+    // us slower with parts, the merge launch unpaid for; 17 steps ran 22%
+    // faster.)
     // (Choosing the parts by the rounds they take, so that launches of more
     // than half a round split too, was slower: a part's fixed costs of Q
     // loads, pipeline fill, half merge and partial store outweigh it.)
-    if (allow_parts && head_dim == 128 && geo.grid > 0) {
-      const long long steps = ((long long)max_kv_len + kBN - 1) / kBN;
+    const long long steps = ((long long)max_kv_len + kBN - 1) / kBN;
+    if (allow_parts && geo.grid > 0 && steps >= kMinPartedSteps) {
       long long parts = std::min<long long>(kCUs / geo.grid, kMaxKeyParts);
-      parts = std::min<long long>(parts, steps / 2);
+      parts = std::min<long long>(parts, steps / kMinPartSteps);
       if (parts > 1) {
         geo.parts = (int)parts;
         geo.grid *= parts;
@@ -1327,10 +1330,15 @@ hipError_t launch_prefill_paged_attn(const AttnLaunch& a, hipStream_t stream) {
   const dim3 grid((unsigned)geo.grid);
   if (geo.parts > 1) {
     // key parts on more work-groups, then the merge of their partials
-    hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<128, true>), grid, dim3(kPPThreads), 0, stream, p);
-    const long long rows_per_block = kThreads / (128 / 4);
+    const long long rows_per_block = kThreads / (a.head_dim / 4);
     const dim3 mgrid((unsigned)((p.part_rows + rows_per_block - 1) / rows_per_block));
-    hipLaunchKernelGGL(prefill_split_merge_kernel<128>, mgrid, dim3(kThreads), 0, stream, p);
+    if (a.head_dim == 128) {
+      hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<128, true>), grid, dim3(kPPThreads), 0, stream, p);
+      hipLaunchKernelGGL(prefill_split_merge_kernel<128>, mgrid, dim3(kThreads), 0, stream, p);
+    } else {
+      hipLaunchKernelGGL((prefill_paged_attn_ppd_split_kernel<64, true>), grid, dim3(kPPThreads), 0, stream, p);
+      hipLaunchKernelGGL(prefill_split_merge_kernel<64>, mgrid, dim3(kThreads), 0, stream, p);
+    }
     return hipGetLastError();
   }
   if (geo.waves == kPPWaves) {

@@ -349,7 +349,7 @@ def test_noalloc_scratch_size_matches_the_header():
     # 3 parts when 85 tiles (4 heads x 32 tokens) leave room for three
     ((1, 2720, 2720, 2720, 4, 1, 128, 256), 3 * 2720 * 4 * 130 * 4),
     ((1, 1024, 1024, 3072, 32, 8, 128, 256), 0),        # a full round of tiles: no parts
-    ((1, 100, 100, 1000, 8, 2, 64, 256), 0),            # head_dim 64: no parts
+    ((1, 100, 100, 1000, 8, 2, 64, 256), 4 * 100 * 8 * 66 * 4),   # head_dim 64: (D + 2) = 66
     ((1, 100, 100, 100, 8, 2, 128, 256), 0),            # two key steps: no parts
     ((0, 0, 0, 0, 8, 2, 128, 256), 0),
     ((-1, 100, 100, 1000, 8, 2, 128, 256), -1),

@@ -2,7 +2,7 @@
 split every tile's keys into parts on separate work-groups and merge the
 partial results (log-sum-exp weights) in a second kernel.
 
-Each case is compared element by element with the float64 oracle (max-abs
+Head dims 64 and 128.  Each case is compared element by element with the float64 oracle (max-abs
 <= 2e-2, mean-abs <= 2e-3) and with the plain cs_prefill_paged_attn on the
 same inputs; the launches are checked to really take key parts.  Cases: the
 one-GPU shard of the 70B-shape serving step (8 query / 1 KV head, through
@@ -73,25 +73,27 @@ CASES = {
     # steps than parts, so some parts hold no step of theirs
     "parts_without_steps": ([3000, 5], [Invocation(0, 40), Invocation(1, 3), Invocation(1, 60)], 8, 2),
     # a miss: early rows see only the first keys, masked in every later part
-    "miss_rows_masked_in_later_parts": ([0, 700], [Invocation(0, 300), Invocation(1, 1)], 8, 8),
+    "miss_rows_masked_in_later_parts": ([0, 1100], [Invocation(0, 300), Invocation(1, 1)], 8, 8),
     "single_token_suffixes": ([1500, 33], [Invocation(0, 1), Invocation(1, 1), Invocation(0, 1)], 16, 2),
     "gqa8_one_kv_head": ([4096], [Invocation(0, 512)], 8, 1),
 }
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
 @pytest.mark.parametrize("name", sorted(CASES))
-def test_key_parts_match_oracle(name):
+def test_key_parts_match_oracle(name, head_dim):
     anchors, invs, hq, hkv = CASES[name]
-    wl = build_workload(name, 71, anchors, invs, num_q_heads=hq, num_kv_heads=hkv, head_dim=128,
+    wl = build_workload(name, 71, anchors, invs, num_q_heads=hq, num_kv_heads=hkv, head_dim=head_dim,
                         num_blocks=1024)
     check_parts(wl)
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
 @pytest.mark.parametrize("poison", ["slot_zero_nan", "nan_inf_tails"])
-def test_key_parts_ignore_poisoned_positions(poison):
+def test_key_parts_ignore_poisoned_positions(poison, head_dim):
     invs = [Invocation(0, 37), Invocation(1, 90), Invocation(0, 5)]
     wl = build_workload("kp_" + poison, 6, [1061, 200], invs, num_q_heads=32, num_kv_heads=8,
-                        head_dim=128, num_blocks=512)
+                        head_dim=head_dim, num_blocks=512)
     if poison == "slot_zero_nan":
         poison_slot_zero(wl)
     else:
