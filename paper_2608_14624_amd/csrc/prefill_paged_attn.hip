@@ -114,7 +114,7 @@ struct Params {
   // rest take the two 128-row halves of the tiles pp_grid, pp_grid + 1, ...
   // (span = the ping-pong tile's tokens)
   long long pp_grid;
-  // stacked mode only
+  // shared_prefix_partials_kernel only (ws_o / ws_ml: also the key parts)
   const int32_t* cu_groups;     // [num_groups + 1] sequence range of each group
   const int32_t* shared_lens;   // [num_groups] shared prefix tokens (multiple of 16)
   int row_tiles;                // 128-row tiles of the largest group

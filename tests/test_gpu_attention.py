@@ -347,7 +347,7 @@ def test_wide_and_small_launches_agree(P, hq, hkv, d):
     invs = [Invocation(i % 3, 300 + 37 * i) for i in range(16)]
     wl = build_workload("wide", 12, [520, 77, 1200], invs, num_q_heads=hq, num_kv_heads=hkv,
                         head_dim=d, num_blocks=4096)
-    print(f"[case] wide vs four-wave hq={hq} hkv={hkv} d={d} total_q={wl.total_q}", flush=True)
+    print(f"[case] wide vs split launch hq={hq} hkv={hkv} d={d} total_q={wl.total_q}", flush=True)
     dw = pipeline.DeviceWorkload(wl)
     dw.attention()
     first = pipeline.SubBatch(dw, 0, 1)
