@@ -76,6 +76,9 @@ CASES = {
     "miss_rows_masked_in_later_parts": ([0, 1100], [Invocation(0, 300), Invocation(1, 1)], 8, 8),
     "single_token_suffixes": ([1500, 33], [Invocation(0, 1), Invocation(1, 1), Invocation(0, 1)], 16, 2),
     "gqa8_one_kv_head": ([4096], [Invocation(0, 512)], 8, 1),
+    # tiles of 1 to 51 steps (and empty ones): parts of very unequal length
+    "unequal_tiles": ([3000, 50, 700], [Invocation(i % 3, n) for i, n in
+                                        enumerate([1, 37, 120, 260, 5, 90])], 8, 4),
 }
 
 
