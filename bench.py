@@ -698,6 +698,11 @@ def main():
                     help="run the plain cs_prefill_paged_attn; by default the attention runs "
                          "cs_prefill_paged_attn_ws, which splits launches too small to fill the "
                          "GPU into key parts (launches of a round or more are unchanged)")
+    ap.add_argument("--overlap", action="store_true",
+                    help="serving step: consecutive agents' attention launches alternate between "
+                         "two streams, so one launch's last round runs beside the next one's "
+                         "first (known order only; the per-launch events still time launches "
+                         "one after another)")
     ap.add_argument("--policy", default="order", choices=("order", "scout"),
                     help="prefetch target: the next agent in dispatch order (default) or the "
                          "control plane's between-step decision (cs_scout_*); the warmup "
@@ -763,13 +768,16 @@ def main():
         policy = None
         if args.policy == "scout":
             policy = pipeline.ScoutPolicy(wl, sorted({inv.agent for inv in wl.invocations}))
-        pipe = pipeline.AgentPipeline(dw, policy=policy)
+        pipe = pipeline.AgentPipeline(dw, policy=policy, overlap=args.overlap)
         pipe.stage_first()
         n_launch = len(pipe.agents)
         step_flops, step_bytes, warm = pipe.flops, pipe.prefetch_bytes, pipe.step
+        # the per-launch events time launches one after another, so with
+        # --overlap they come from a pipeline of the same work without it
+        pipe_ev = pipe if not pipe.overlap else pipeline.AgentPipeline(dw)
     else:
         # no CPU-tier blocks: the whole batch is one attention launch
-        pipe = None
+        pipe = pipe_ev = None
         n_launch = 1
         step_flops, step_bytes, warm = wl.flops(), 0, dw.attention
     for _ in range(args.warmup):
@@ -789,10 +797,11 @@ def main():
             a_ev[si][0][1].record(main_stream)
             return
         # AgentPipeline.step with events around each launch
-        pipe.step(timing=list(zip(p_ev[si], a_ev[si])))
+        pipe_ev.step(timing=list(zip(p_ev[si], a_ev[si])))
 
     torch.cuda.synchronize()
-    hits0, misses0 = (pipe.hits, pipe.misses) if pipe is not None else (0, 0)
+    pipes = [] if pipe is None else ([pipe] if pipe_ev is pipe else [pipe, pipe_ev])
+    hits0, misses0 = sum(q.hits for q in pipes), sum(q.misses for q in pipes)
     # the timed region: exactly `steps` serving steps, nothing recorded inside
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -903,7 +912,9 @@ def main():
                                "same steps after the timed region"},
         "prefetch": prefetch,
         "prefetch_policy": None if pipe is None else {
-            "name": args.policy, "hits": pipe.hits - hits0, "misses": pipe.misses - misses0},
+            "name": args.policy, "hits": sum(q.hits for q in pipes) - hits0,
+            "misses": sum(q.misses for q in pipes) - misses0,
+            "launches_overlapped": pipe.overlap},
         "kernel_sha": khash,
         "library_digest": ops.source_digest(),
         "source_digest": build.source_digest(),

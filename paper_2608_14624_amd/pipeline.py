@@ -178,10 +178,14 @@ class AgentPipeline:
 
     Requires the invocations to be packed grouped by agent (each agent's
     invocations contiguous) and at least two agents.  ``policy``: None for the
-    known dispatch order, or a :class:`ScoutPolicy`.
+    known dispatch order, or a :class:`ScoutPolicy`.  ``overlap`` (known order
+    only): consecutive agents' attention launches alternate between the
+    current stream and a second one, so that one launch's last round can run
+    beside the next launch's first; each still waits only for its own
+    prefetch, and the pass ends on the current stream.
     """
 
-    def __init__(self, dw, side_stream=None, policy=None):
+    def __init__(self, dw, side_stream=None, policy=None, overlap=False):
         wl = dw.wl
         agents = [inv.agent for inv in wl.invocations]
         order = []
@@ -215,6 +219,8 @@ class AgentPipeline:
                 assert i1 - i0 == len(idx), "prefetch blocks must be grouped by agent"
                 self.prefetch[a] = (dw.host_k[i0:i1], dw.host_v[i0:i1], dw.prefetch_dst[i0:i1])
         self.side = side_stream if side_stream is not None else torch.cuda.Stream(dw.device)
+        self.overlap = overlap and policy is None
+        self.alt = torch.cuda.Stream(dw.device) if self.overlap else None
         self.events = {a: torch.cuda.Event() for a in order}       # prefetch done
         self.attn_done = {a: torch.cuda.Event() for a in order}    # last reader done
         # known order only: the previous pass ended / the first agent's
@@ -247,7 +253,14 @@ class AgentPipeline:
         main = torch.cuda.current_stream(self.dw.device)
         n = len(self.agents)
         known = self.policy is None
+
+        def turn_stream(t):
+            return self.alt if self.overlap and t % 2 == 1 else main
+
+        if self.overlap:
+            self.alt.wait_stream(main)      # work enqueued before this pass
         for k, a in enumerate(self.agents):
+            s_k = turn_stream(k)
             nxt = self.agents[(k + 1) % n]
             target = nxt if known else self.policy.on_turn(a)
             (p0, p1), (a0, a1) = timing[k] if timing is not None else ((None, None),) * 2
@@ -275,19 +288,21 @@ class AgentPipeline:
                 p0.record(self.side)
                 p1.record(self.side)
             if a0 is not None:
-                a0.record(main)
-            self.batches[k].attention(stream=main)
+                a0.record(s_k)
+            self.batches[k].attention(stream=s_k)
             if a1 is not None:
-                a1.record(main)
+                a1.record(s_k)
             if not known:
                 self.attn_done[a].record(main)
             elif k == 0:
-                self.first_done.record(main)
+                self.first_done.record(s_k)
             if known and k == n - 1:
+                if self.overlap:
+                    main.wait_stream(self.alt)   # the pass ends with every launch
                 self.pass_done.record(main)
             if target == nxt:
                 self.hits += 1
-                main.wait_event(self.events[nxt])
+                turn_stream((k + 1) % n).wait_event(self.events[nxt])
             else:
                 # a miss: the next agent's blocks come in on the critical path
                 # (after any side-stream write still in flight)

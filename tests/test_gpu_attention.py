@@ -207,15 +207,18 @@ def test_agent_batch_full(P):
     assert mx <= MAX_ABS and mean <= MEAN_ABS
 
 
-def test_llama70b_prefetch_pipeline_full(P):
+@pytest.mark.parametrize("overlap", [False, True])
+def test_llama70b_prefetch_pipeline_full(P, overlap):
     """The benchmark's launch configuration: per-agent attention with the next
-    agent's CPU-tier blocks prefetched on a side stream; every output element
-    against the oracle."""
+    agent's CPU-tier blocks prefetched on a side stream (and with consecutive
+    agents' launches on two streams); every output element against the
+    oracle.  The prefetched slots start as NaN, so an attention launch that
+    ran before its agent's prefetch had landed would show."""
     _, pipeline = P
     wl = make_config("llama70b_prefetch")
-    print(f"[case] llama70b_prefetch pipeline total_q={wl.total_q}", flush=True)
+    print(f"[case] llama70b_prefetch pipeline total_q={wl.total_q} overlap={overlap}", flush=True)
     dw = pipeline.DeviceWorkload(wl)
-    pipe = pipeline.AgentPipeline(dw)
+    pipe = pipeline.AgentPipeline(dw, overlap=overlap)
     pipe.stage_first()
     dw.out.fill_(float("nan"))
     pipe.step()

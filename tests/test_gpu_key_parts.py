@@ -104,15 +104,17 @@ def test_key_parts_ignore_poisoned_positions(poison, head_dim):
     check_parts(wl)
 
 
-def test_tp8_shard_pipeline_full():
+@pytest.mark.parametrize("overlap", [False, True])
+def test_tp8_shard_pipeline_full(overlap):
     """One GPU's shard of the 70B-shape serving step (8 query / 1 KV head):
     the per-agent launches of up to half a round of tiles take key parts (two
     or four here), with the next agent's prefetch beside them, as the
-    benchmark runs them."""
+    benchmark runs them (and with consecutive launches on two streams, each
+    with its own workspace)."""
     from paper_2608_14624_amd import ops, pipeline
     wl = make_config("llama70b_prefetch_tp8")
     dw = pipeline.DeviceWorkload(wl, workspace="auto")
-    pipe = pipeline.AgentPipeline(dw)
+    pipe = pipeline.AgentPipeline(dw, overlap=overlap)
     parts = [parts_of(ops, wl, b.lo, b.hi) for b in pipe.batches]
     print(f"[case] llama70b_prefetch_tp8 key parts per agent launch: {parts}", flush=True)
     assert max(parts) >= 2
