@@ -218,6 +218,23 @@ def test_cascade_decode_without_sharing_equals_paged_decode():
     check(ref, oracle_decode(q, seq_lens, wl.block_tables, wl), "paged decode vs oracle")
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_decode_and_cascade_with_peaky_logits(d):
+    """Queries scaled up 8x (logits in the tens of log2 units): the decode
+    kernel's per-chunk max and rescale, and the cascade's partials merged
+    with widely different maxima, stay within the bounds."""
+    invs = [Invocation(0, 5), Invocation(0, 900), Invocation(1, 40), Invocation(1, 1)]
+    wl = build_workload("peaky_dec", 47, [1500, 200], invs, num_q_heads=16, num_kv_heads=4,
+                        head_dim=d, num_blocks=1024, q_gain=8.0)
+    print(f"[case] peaky decode / cascade d={d} kv_lens={wl.kv_lens.tolist()}", flush=True)
+    q, seq_lens = decode_view(wl)
+    check(run_decode(wl), oracle_decode(q, seq_lens, wl.block_tables, wl), "decode vs oracle")
+    q, seq_lens, bt, cv = grouped_batch(wl)
+    got = run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"],
+                      cv["max_group_seqs"], cv["max_shared_len"])
+    check(got, oracle_decode(q, seq_lens, bt, wl), "cascade vs oracle")
+
+
 def test_cascade_decode_batch_config():
     wl = make_config("decode_batch")
     q, seq_lens, bt, cv = grouped_batch(wl)

@@ -92,6 +92,17 @@ def test_key_parts_match_oracle(name, head_dim):
 
 
 @pytest.mark.parametrize("head_dim", [64, 128])
+def test_key_parts_with_peaky_logits(head_dim):
+    """Queries scaled up 8x (logits in the tens of log2 units): the parts'
+    maxima differ widely, and the merge's log-sum-exp weights must still
+    give the oracle's result."""
+    wl = build_workload("kp_peaky", 73, [2000, 300], [Invocation(0, 120), Invocation(1, 60)],
+                        num_q_heads=8, num_kv_heads=2, head_dim=head_dim, num_blocks=1024,
+                        q_gain=8.0)
+    check_parts(wl)
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
 @pytest.mark.parametrize("poison", ["slot_zero_nan", "nan_inf_tails"])
 def test_key_parts_ignore_poisoned_positions(poison, head_dim):
     invs = [Invocation(0, 37), Invocation(1, 90), Invocation(0, 5)]
