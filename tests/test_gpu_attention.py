@@ -207,6 +207,24 @@ def test_agent_batch_full(P):
     assert mx <= MAX_ABS and mean <= MEAN_ABS
 
 
+def test_agent_batch_tp8_shard_full(P):
+    """One GPU's shard of agent_batch under an 8-way KV-head split (4 query
+    heads / 1 KV head): one launch of 1024 ping-pong tiles, all of them on
+    the one KV head, called with a workspace as the benchmark calls it (a
+    launch this large takes no key parts); every output element."""
+    _, pipeline = P
+    wl = make_config("agent_batch_tp8")
+    print(f"[case] agent_batch_tp8 total_q={wl.total_q} Hq={wl.num_q_heads} Hkv={wl.num_kv_heads}",
+          flush=True)
+    dw = pipeline.DeviceWorkload(wl, workspace="auto")
+    dw.attention()
+    torch.cuda.synchronize()
+    mx, mean = compare_full(dw.out_bits(), oracle_full(wl))
+    print(f"    all {wl.total_q * wl.num_q_heads} rows: max_abs={mx:.3e} mean_abs={mean:.3e}",
+          flush=True)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
 @pytest.mark.parametrize("overlap", [False, True])
 def test_llama70b_prefetch_pipeline_full(P, overlap):
     """The benchmark's launch configuration: per-agent attention with the next
