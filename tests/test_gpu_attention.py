@@ -389,6 +389,53 @@ def test_wide_and_small_launches_agree(P, hq, hkv, d):
     assert mx <= MAX_ABS and mean <= MEAN_ABS
 
 
+LOOSE = {
+    # name: (extra max_q_len, extra max_kv_len, workspace, expected kernel,
+    #        key parts expected): with exact bounds this batch is a split
+    #        launch of 112 tiles without parts
+    "split_with_key_parts": (56, 3000, "auto", 0, True),
+    "ping_pong_mostly_empty": (800, 3000, None, 1, False),
+}
+
+
+@pytest.mark.parametrize("name", sorted(LOOSE))
+def test_loose_host_bounds(P, name):
+    """max_q_len and max_kv_len only need to bound the lengths (>=): bounds
+    far above them size a launch with token tiles past every suffix (they
+    leave at once), may switch the kernel, and with a workspace cut key
+    parts whose later ranges hold no key of any sequence.  The output still
+    matches the oracle on every element."""
+    from paper_2608_14624_amd import ops
+    extra_q, extra_kv, workspace, want_kernel, want_parts = LOOSE[name]
+    invs = [Invocation(0, 90), Invocation(1, 33), Invocation(0, 1), Invocation(1, 200)]
+    wl = build_workload("loose", 77, [700, 260], invs, num_q_heads=16, num_kv_heads=4,
+                        head_dim=128, num_blocks=512)
+    mq, mk = wl.max_q_len + extra_q, wl.max_kv_len + extra_kv
+    kernel, grid, _ = ops.prefill_launch_shape(wl.batch, mq, 16, 4)
+    need = ops.prefill_workspace_bytes(wl.batch, wl.total_q, mq, mk, 16, 4, 128)
+    print(f"[case] loose bounds {name}: max_q_len {wl.max_q_len}->{mq}, max_kv_len "
+          f"{wl.max_kv_len}->{mk}, kernel {kernel}, grid {grid}, workspace {need} B", flush=True)
+    assert kernel == want_kernel and (need > 0) == want_parts
+    # the block table widened so that max_blocks_per_seq * 16 covers the bound
+    bt = np.zeros((wl.batch, -(-mk // 16)), np.int32)
+    bt[:, :wl.block_tables.shape[1]] = wl.block_tables
+    dev = torch.device("cuda")
+
+    def bf16(a):
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+    q = bf16(wl.q)
+    out = torch.full_like(q, float("nan"))
+    ops.cs_prefill_paged_attn(q, bf16(wl.k_pool), bf16(wl.v_pool), torch.from_numpy(bt).to(dev),
+                              torch.from_numpy(wl.prefix_lens).to(dev),
+                              torch.from_numpy(wl.cu_q_lens).to(dev), out, max_q_len=mq,
+                              max_kv_len=mk, scale=wl.scale, workspace=workspace)
+    torch.cuda.synchronize()
+    got = out.view(torch.int16).cpu().numpy().view(np.uint16)
+    mx, mean = compare_full(got, oracle_full(wl))
+    print(f"    max_abs={mx:.3e} mean_abs={mean:.3e}", flush=True)
+    assert mx <= MAX_ABS and mean <= MEAN_ABS
+
+
 def test_hit_rows_match_miss_rows(P):
     # the same prompt served as a hit and as a miss
     for prefix, suffix in ((256, 64), (37, 100), (1000, 1)):

@@ -118,7 +118,7 @@ def rest_bound(seq_lens, cu, shared):
 
 
 def run_cascade(wl, q, seq_lens, bt, cu, shared, max_group_seqs, max_shared_len, workspace=None,
-                max_rest_len=None):
+                max_rest_len=None, max_seq_len=None):
     from paper_2608_14624_amd import ops
     qd = dev_bf16(q)
     out = torch.full_like(qd, float("nan"))
@@ -126,7 +126,9 @@ def run_cascade(wl, q, seq_lens, bt, cu, shared, max_group_seqs, max_shared_len,
                                torch.from_numpy(bt).cuda(), torch.from_numpy(seq_lens).cuda(),
                                torch.from_numpy(np.asarray(cu, np.int32)).cuda(),
                                torch.from_numpy(np.asarray(shared, np.int32)).cuda(), out,
-                               max_seq_len=int(seq_lens.max()), max_group_seqs=max_group_seqs,
+                               max_seq_len=(int(seq_lens.max()) if max_seq_len is None
+                                            else max_seq_len),
+                               max_group_seqs=max_group_seqs,
                                max_shared_len=max_shared_len,
                                max_rest_len=(rest_bound(seq_lens, cu, shared)
                                              if max_rest_len is None else max_rest_len),
@@ -166,6 +168,37 @@ def test_cascade_decode_matches_oracle(name):
     got = run_cascade(wl, q, seq_lens, bt, cv["cu_groups"], cv["shared_lens"],
                       cv["max_group_seqs"], cv["max_shared_len"])
     check(got, oracle_decode(q, seq_lens, bt, wl), "vs oracle")
+
+
+def test_cascade_decode_with_loose_host_bounds():
+    """max_group_seqs, max_shared_len, max_rest_len and max_seq_len only need
+    to bound the batch: with each well above it the launches carry row
+    tiles, shared-prefix chunks and own-key segments that hold nothing (they
+    leave at once) and the workspace has more partial slots than any row
+    uses.  The merge takes each row's own partial count, so the result is
+    bitwise the one of the exact bounds, and matches the oracle."""
+    # 12 sequences of 3 agents plus a miss; G = 16, so the loosest
+    # max_group_seqs (the batch) gives a second, empty row tile
+    invs = [Invocation(i % 3, 1 + (i * 53) % 400) for i in range(12)] + [Invocation(1, 30, False)]
+    wl = build_workload("loose_cascade", 43, [1100, 530, 700], invs, num_q_heads=32,
+                        num_kv_heads=2, head_dim=128, num_blocks=1024)
+    q, seq_lens, bt, cv = grouped_batch(wl)
+    cu, shared = cv["cu_groups"], cv["shared_lens"]
+    exact = run_cascade(wl, q, seq_lens, bt, cu, shared, cv["max_group_seqs"], cv["max_shared_len"])
+    max_seq = int(seq_lens.max()) + 4096
+    wide = np.zeros((len(seq_lens), -(-max_seq // 16)), np.int32)
+    wide[:, :bt.shape[1]] = bt
+    bounds = dict(max_group_seqs=len(seq_lens),
+                  max_shared_len=cv["max_shared_len"] + 2048,
+                  max_rest_len=rest_bound(seq_lens, cu, shared) + 2500, max_seq_len=max_seq)
+    print(f"[case] cascade with loose bounds {bounds} (exact: {cv['max_group_seqs']}, "
+          f"{cv['max_shared_len']}, {rest_bound(seq_lens, cu, shared)}, {int(seq_lens.max())})",
+          flush=True)
+    loose = run_cascade(wl, q, seq_lens, wide, cu, shared, bounds["max_group_seqs"],
+                        bounds["max_shared_len"], max_rest_len=bounds["max_rest_len"],
+                        max_seq_len=bounds["max_seq_len"])
+    assert np.array_equal(loose, exact)
+    check(loose, oracle_decode(q, seq_lens, bt, wl), "loose bounds vs oracle")
 
 
 def test_cascade_decode_two_row_tiles_and_empty_private_part():
