@@ -75,6 +75,12 @@ EDGE = {
     "group2": ([33], [Invocation(0, 97)], 4, 2, 128, {}),
     "group8": ([200], [Invocation(0, 65), Invocation(0, 31)], 16, 2, 128, {}),
     "group3": ([17], [Invocation(0, 45)], 6, 2, 64, {}),
+    # groups of 5, 6, 16 and 32 query heads per KV head: one, two and four
+    # heads per tile (five and six split over several head tiles)
+    "group5": ([23], [Invocation(0, 33)], 5, 1, 128, {}),
+    "group6": ([40], [Invocation(0, 77), Invocation(0, 2)], 12, 2, 128, {}),
+    "group16_mqa_d64": ([100], [Invocation(0, 50), Invocation(0, 9)], 16, 1, 64, {}),
+    "group32_mqa": ([300], [Invocation(0, 40)], 32, 1, 128, {}),
     "zero_prefix_hit": ([0], [Invocation(0, 77)], 8, 2, 128, {}),
     "peaky_logits": ([90], [Invocation(0, 70)], 8, 2, 128, {"q_gain": 8.0}),
     "long_ragged_tile": ([1000], [Invocation(0, 257), Invocation(0, 129)], 32, 8, 128, {}),
@@ -358,7 +364,8 @@ def test_run_to_run_determinism(P):
         assert torch.equal(a.view(torch.int16), dw.out.view(torch.int16))
 
 
-@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 8, 64), (12, 4, 128), (8, 8, 128)])
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (16, 8, 64), (12, 4, 128), (8, 8, 128),
+                                     (24, 4, 128), (32, 2, 64)])
 def test_wide_and_small_launches_agree(P, hq, hkv, d):
     """A batch large enough for the 8-wave ping-pong kernel, and its first
     invocation alone (a launch below one work-group per CU, whose tiles run
